@@ -1,0 +1,34 @@
+"""CPU oracle for the ring-attention hot path: TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, float64 NumPy implementation of what the HIP library computes, written
+from the paper (Liu, Zaharia, Abbeel, "Ring Attention with Blockwise Transformers for
+Near-Infinite Context", arXiv 2310.01889).  Only the test suite, the smoke check in
+``__graft_entry__.py`` and the ``cpu_baseline`` leg of ``bench.py`` may import it; the
+product path (``paper_2310_01889_amd``) never does, and shares no code with it.
+
+Modules
+  attention  -- exact softmax attention from its definition (Section 2 equation),
+                forward and backward, materialising the score matrix (row-chunked).
+  ring       -- the ring schedule of Section 3 / Appendix A: N virtual hosts, each
+                holding one query block; key/value blocks (and, in the backward pass,
+                their gradients) are physically rotated host i -> host i+1 after
+                every step, and each block is folded in with running max /
+                numerator / denominator statistics, tile by tile.
+  brute      -- scalar triple loops (no BLAS) for tiny shapes.
+  ffn        -- position-wise feed-forward network (Section 2 equation) with the
+                activations used here (GeLU-erf, ReLU, GeLU-tanh), its blockwise
+                form (Section 2, "Blockwise Parallel Transformers"), and the
+                projection ``y = x w (+ residual)``; forward and backward.
+  layer      -- one transformer layer as Algorithm 1 composes it: projections,
+                ring attention, output projection with residual, blockwise FFN with
+                residual; forward and backward.
+
+Every function takes and returns float64 arrays.  Inputs in bf16 are passed in already
+rounded (the exact values the GPU sees), then upcast.
+
+Parity status: attention forward/backward, ring bookkeeping and FFN are pinned by the
+tests in tests/test_oracle_*.py (closed forms, invariants, brute force, finite
+differences, library routines).  The layer composition is pinned only to the
+composition defined in ``layer`` (the paper does not fix norms, biases or the
+activation of that layer): for it, parity unpinned beyond its parts.
+"""

@@ -1,0 +1,82 @@
+"""Planted mistakes in the oracle must be caught by its pins (CPU only).
+
+Each case patches one plausible slip into a copy of an oracle function (a dropped
+scale, an off-by-one mask, a missing rescale, a wrong sign, a dropped derivative
+term, a transposed operand) and re-runs the pin that should catch it.
+"""
+import numpy as np
+import pytest
+
+from oracle import attention as A
+from oracle import ffn as F
+from oracle import ring as R
+import tests.test_oracle_attention as TA
+import tests.test_oracle_ffn as TF
+import tests.test_oracle_ring as TR
+
+
+def _fails(check, *args):
+    with pytest.raises(AssertionError):
+        check(*args)
+
+
+def test_dropped_scale_is_caught(monkeypatch):
+    orig = A._masked_scores
+    monkeypatch.setattr(A, "_masked_scores", lambda qh, kh, scale, c, p, r: orig(qh, kh, 1.0, c, p, r))
+    _fails(TA.test_naive_matches_brute_force, 5, 3, True)
+    _fails(TA.test_naive_matches_torch_sdpa_fp64, True)
+
+
+def test_off_by_one_causal_mask_is_caught(monkeypatch):
+    def masked(qh, kh, scale, causal, q_pos0, r0):
+        s = (qh @ kh.T) * scale
+        qpos = q_pos0 + r0 + np.arange(qh.shape[0])[:, None]
+        kpos = np.arange(kh.shape[0])[None, :]
+        return np.where(kpos > qpos + 1, -np.inf, s) if causal else s
+    monkeypatch.setattr(A, "_masked_scores", masked)
+    _fails(TA.test_first_causal_token)
+    _fails(TA.test_zero_query_gives_prefix_mean)
+
+
+def test_missing_numerator_rescale_is_caught(monkeypatch):
+    orig_exp = np.exp
+
+    def fold(state, q, kb, vb, qp, kp, causal, scale, qc, kc):
+        # fold every tile with the max of its own tile only: correction dropped
+        mx, num, den = state
+        for q0 in range(0, q.shape[1], qc):
+            q1 = min(q.shape[1], q0 + qc)
+            for k0 in range(0, kb.shape[1], kc):
+                k1 = min(kb.shape[1], k0 + kc)
+                vis = R._visible(qp + np.arange(q0, q1), kp + np.arange(k0, k1), causal)
+                if not vis.any():
+                    continue
+                s = np.where(vis[None, None], R._scores(q[:, q0:q1], kb[:, k0:k1], scale), -np.inf)
+                m_new = np.maximum(mx[:, :, q0:q1], s.max(axis=3))
+                p = orig_exp(s - m_new[..., None])
+                den[:, :, q0:q1] = den[:, :, q0:q1] + p.sum(axis=3)
+                num[:, q0:q1] = num[:, q0:q1] + np.einsum("bhqk,bkhd->bqhd", p, vb[:, k0:k1])
+                mx[:, :, q0:q1] = m_new
+    monkeypatch.setattr(R, "_fold_block_fwd", fold)
+    _fails(TR.test_ring_forward_equals_naive, 4, True)
+
+
+def test_wrong_sign_in_softmax_gradient_is_caught(monkeypatch):
+    def bwd(q, k, v, do, causal, scale=None, q_offset=0, row_chunk=1024):
+        dq, dk, dv = orig(q, k, v, do, causal, scale, q_offset, row_chunk)
+        return -dq, -dk, dv
+    orig = A.attention_bwd
+    monkeypatch.setattr(A, "attention_bwd", bwd)
+    _fails(TA.test_backward_finite_differences, True)
+
+
+def test_dropped_gelu_derivative_term_is_caught(monkeypatch):
+    orig = F.act_grad
+    monkeypatch.setattr(F, "act_grad", lambda h, act: 0.5 * (1 + np.tanh(h)) if act == F.GELU_ERF else orig(h, act))
+    _fails(TF.test_ffn_backward_finite_differences)
+
+
+def test_transposed_weight_gradient_is_caught(monkeypatch):
+    orig = F.linear_bwd
+    monkeypatch.setattr(F, "linear_bwd", lambda x, w, dy: (orig(x, w, dy)[0], (np.asarray(dy).T @ np.asarray(x)).T[::-1]))
+    _fails(TF.test_linear_forward_backward)
