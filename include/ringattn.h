@@ -1,0 +1,172 @@
+/*
+ * ringattn.h -- C ABI of the MI355X (gfx950) ring-attention library.
+ *
+ * Ring Attention with Blockwise Transformers (Liu, Zaharia, Abbeel; arXiv 2310.01889):
+ * one host's share of exact blockwise self-attention.  The sequence of length S is split
+ * into n_hosts equal blocks of c = S / n_hosts tokens; host i keeps query block i
+ * resident while key/value blocks reach it in ring order, block (i - t) mod n_hosts at
+ * step t (Section 3, "Ring-Based Blockwise Attention"; Appendix A forward code).  Each
+ * block is folded into the output with running row maximum, running denominator and a
+ * rescaled output accumulator.  The backward pass (Appendix A backward code) accumulates
+ * dQ on the host and dK/dV with the rotating block.  A blockwise feed-forward network
+ * (Section 2 equation; Algorithm 1) follows the attention of the same query block.
+ *
+ * On one GPU the ring is virtual: all hosts' blocks live in device memory; each call
+ * runs n_hosts ring steps, each one kernel launch covering every host that has work at
+ * that step, and before each step the blocks that every host will need next are copied
+ * into a per-host receive buffer (double buffer) on a library-owned side stream,
+ * overlapping the compute of the current step.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers unless stated.  The caller allocates and owns every
+ *     input and output and keeps them alive until `stream` has finished the call.  The
+ *     library keeps no pointer after returning.
+ *   - Tensors are dense row-major.  q, k, v, o, dO, dq, dk, dv: [B, S, H, D] (batch,
+ *     position, head, dim per head; the layout of the paper's code).  lse: float32
+ *     [B, H, S], holding max + ln(denominator) of the scaled scores (natural log).
+ *   - "bf16" tensors hold IEEE bfloat16 (hip_bfloat16 / torch.bfloat16).  Products are
+ *     taken in bf16 with float32 accumulation (the paper's float32-logits option);
+ *     softmax statistics, accumulators and weight gradients are float32; outputs are
+ *     rounded to bf16 with round-to-nearest-even.
+ *   - Scores are scaled by 1/sqrt(D) (Section 2 equation).  With causal != 0, query at
+ *     global position p sees key at global position p' iff p' <= p; masked keys
+ *     contribute exactly zero and fully masked blocks are skipped.
+ *   - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t; NULL means
+ *     the legacy default stream).  Work on the side stream is joined back to `stream`
+ *     by events, so callers see single-stream semantics.  Distinct streams may be used
+ *     from distinct threads concurrently.
+ *   - Workspace (receive buffers, float32 accumulators) is allocated stream-ordered on
+ *     `stream` and released at the end of the call.
+ *   - Return value: RA_OK or an ra_status error code.  Arguments are validated before
+ *     anything is enqueued: on error nothing is enqueued and outputs are untouched.
+ *     ring_attn_last_error() describes the last error on the calling thread.  NaN or
+ *     Inf inputs are not checked; they propagate.
+ *
+ * Supported shapes: D in {64, 128}; 1 <= n_hosts <= 64; S % n_hosts == 0; the block
+ * c = S / n_hosts a multiple of 128 (bf16 attention) or 64 (float32 attention); B, H >= 1;
+ * B * S * H * D < 2^31 elements per tensor.
+ */
+#ifndef RINGATTN_H
+#define RINGATTN_H
+
+#include <hip/hip_runtime.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RA_OK = 0,
+  RA_EINVAL = 1,        /* null pointer, non-positive size, bad enum value         */
+  RA_EUNSUPPORTED = 2,  /* shape outside the supported set listed above            */
+  RA_EHIP = 3,          /* a HIP launch, copy or event call failed                 */
+  RA_ENOMEM = 4         /* workspace allocation failed                             */
+} ra_status;
+
+/* Activation of the feed-forward network. */
+typedef enum { RA_ACT_GELU_ERF = 0, RA_ACT_RELU = 1, RA_ACT_GELU_TANH = 2 } ra_act;
+
+/*
+ * Ring attention forward (Section 3; Appendix A forward code), bf16.
+ *   q, k, v  in   bf16 [B, S, H, D]
+ *   o        out  bf16 [B, S, H, D]      softmax(q k^T / sqrt(D)) v, row by row
+ *   lse      out  f32  [B, H, S]         log-sum-exp of each query's scaled scores
+ *   n_hosts       number of virtual hosts of the ring; block c = S / n_hosts
+ *   causal        0 or 1
+ */
+int ring_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                  int B, int H, int S, int D, int n_hosts, int causal, hipStream_t stream);
+
+/*
+ * Ring attention backward (Appendix A backward code), bf16.
+ *   q, k, v, o, lse   the forward inputs and outputs (o, lse as written by ring_attn_fwd)
+ *   dO        in   bf16 [B, S, H, D]   upstream gradient of o
+ *   dq, dk, dv out bf16 [B, S, H, D]   gradients of sum(dO * o); accumulated in float32
+ *                                      (dq on the host, dk/dv with their rotating block)
+ *                                      and rounded once at the end.
+ */
+int ring_attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                  const void* dO, void* dq, void* dk, void* dv,
+                  int B, int H, int S, int D, int n_hosts, int causal, hipStream_t stream);
+
+/* float32 twins of ring_attn_fwd / ring_attn_bwd: every tensor is float32, products and
+ * accumulation are float32 (no bf16 rounding anywhere). */
+int ring_attn_fwd_f32(const float* q, const float* k, const float* v, float* o, float* lse,
+                      int B, int H, int S, int D, int n_hosts, int causal, hipStream_t stream);
+int ring_attn_bwd_f32(const float* q, const float* k, const float* v, const float* o,
+                      const float* lse, const float* dO, float* dq, float* dk, float* dv,
+                      int B, int H, int S, int D, int n_hosts, int causal, hipStream_t stream);
+
+/*
+ * One host's share of the ring (Section 3; the per-host view of Figure 2 and of the
+ * Appendix A scan), bf16: query block `host_idx` against every key/value block, the
+ * blocks arriving in ring order (host_idx - t) mod n_hosts, step 0 being the host's own
+ * block, each later block prefetched into the host's receive buffer on the side stream.
+ *   q_blk     in   bf16 [B, c, H, D]    query block host_idx (global positions host_idx*c + r)
+ *   k_all, v_all in bf16 [B, S, H, D]   all key/value blocks, S = n_hosts * c
+ *   o_blk     out  bf16 [B, c, H, D]
+ *   lse_blk   out  f32  [B, H, c]
+ */
+int ring_attn_fwd_host(const void* q_blk, const void* k_all, const void* v_all, void* o_blk,
+                       float* lse_blk, int B, int H, int S, int D, int n_hosts, int host_idx,
+                       int causal, hipStream_t stream);
+
+/*
+ * Ring attention forward with an explicit block order, bf16 (checks the permutation
+ * invariance that Section 3 relies on: blocks may be folded in any order).
+ *   kv_order  HOST pointer, int[n_hosts * n_hosts]; row i is the sequence of key/value
+ *             blocks host i folds in, a permutation of 0..n_hosts-1.  Copied before return.
+ * Otherwise as ring_attn_fwd.  Returns RA_EINVAL if a row is not a permutation.
+ */
+int ring_attn_fwd_ordered(const void* q, const void* k, const void* v, void* o, float* lse,
+                          int B, int H, int S, int D, int n_hosts, int causal,
+                          const int* kv_order, hipStream_t stream);
+
+/*
+ * Blockwise feed-forward network (Section 2 equation and "Blockwise Parallel
+ * Transformers"; Algorithm 1's feed-forward step), bf16:
+ *   y = act(x W1 + b1) W2 + b2, computed `block` rows at a time, so the [rows, d_ff]
+ *   intermediate exists for one block only.
+ *   x  in bf16 [T, d_model];  w1 in bf16 [d_model, d_ff];  b1 in bf16 [d_ff] or NULL
+ *   w2 in bf16 [d_ff, d_model];  b2 in bf16 [d_model] or NULL;  y out bf16 [T, d_model]
+ *   act: an ra_act value.   T % block == 0, block % 256 == 0, d_model % 256 == 0,
+ *   d_ff % 256 == 0.
+ */
+int blockwise_ffn(const void* x, const void* w1, const void* b1, const void* w2, const void* b2,
+                  void* y, int T, int d_model, int d_ff, int block, int act, hipStream_t stream);
+
+/*
+ * Backward of blockwise_ffn for upstream dy (bf16 [T, d_model]).  The pre-activation
+ * x W1 + b1 is recomputed block by block (gradient checkpointing, Section 4 setting).
+ *   dx  out bf16 [T, d_model]
+ *   dw1 out f32 [d_model, d_ff], db1 out f32 [d_ff] (may be NULL),
+ *   dw2 out f32 [d_ff, d_model], db2 out f32 [d_model] (may be NULL).
+ * Weight and bias gradients are overwritten (not accumulated into) and kept in float32.
+ */
+int blockwise_ffn_bwd(const void* x, const void* w1, const void* b1, const void* w2,
+                      const void* dy, void* dx, float* dw1, float* db1, float* dw2, float* db2,
+                      int T, int d_model, int d_ff, int block, int act, hipStream_t stream);
+
+/*
+ * Per-block projection used by Algorithm 1 (query/key/value of each input block and the
+ * output projection), bf16:  y = x W (+ residual).
+ *   x in bf16 [T, d_in]; w in bf16 [d_in, d_out]; residual in bf16 [T, d_out] or NULL;
+ *   y out bf16 [T, d_out].  T % block == 0, block % 256 == 0, d_in, d_out % 256 == 0.
+ */
+int blockwise_linear(const void* x, const void* w, const void* residual, void* y, int T,
+                     int d_in, int d_out, int block, hipStream_t stream);
+
+/* Backward of blockwise_linear without residual: dx = dy W^T (bf16 [T, d_in], may be
+ * NULL), dw = x^T dy (f32 [d_in, d_out], overwritten). */
+int blockwise_linear_bwd(const void* x, const void* w, const void* dy, void* dx, float* dw,
+                         int T, int d_in, int d_out, int block, hipStream_t stream);
+
+/* Description of the last error returned on the calling thread ("" if none).  Valid
+ * until the next library call on that thread. */
+const char* ring_attn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RINGATTN_H */

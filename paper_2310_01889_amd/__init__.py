@@ -1,0 +1,217 @@
+"""Python binding of libringattn.so, the MI355X (gfx950) ring-attention library.
+
+Argument marshalling only: every step of the computation runs in the library's HIP
+kernels.  torch supplies device memory and the current HIP stream.  Each function has
+the name of the C entry point it calls (see include/ringattn.h for layouts, ownership
+and error behaviour) and takes torch tensors that live on the current GPU; shapes are
+read from the tensors.  Convenience wrappers that allocate their outputs are provided
+for tests and benchmarks (``attention_fwd``, ``attention_bwd``, ``ffn_fwd``...).
+
+The library is loaded on first use.  If it has not been built, or no GPU is present,
+calls raise: there is no fallback path.
+"""
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "RingAttnError", "library_path", "load", "exported_symbols",
+    "ring_attn_fwd", "ring_attn_bwd", "ring_attn_fwd_f32", "ring_attn_bwd_f32",
+    "ring_attn_fwd_host", "ring_attn_fwd_ordered", "blockwise_ffn", "blockwise_ffn_bwd",
+    "blockwise_linear", "blockwise_linear_bwd", "attention_fwd", "attention_bwd",
+    "ACT_GELU_ERF", "ACT_RELU", "ACT_GELU_TANH",
+]
+
+ACT_GELU_ERF, ACT_RELU, ACT_GELU_TANH = 0, 1, 2
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_SIGS = {
+    "ring_attn_fwd": [_P] * 5 + [_I] * 6 + [_P],
+    "ring_attn_fwd_f32": [_P] * 5 + [_I] * 6 + [_P],
+    "ring_attn_bwd": [_P] * 9 + [_I] * 6 + [_P],
+    "ring_attn_bwd_f32": [_P] * 9 + [_I] * 6 + [_P],
+    "ring_attn_fwd_host": [_P] * 5 + [_I] * 7 + [_P],
+    "ring_attn_fwd_ordered": [_P] * 5 + [_I] * 6 + [_P, _P],
+    "blockwise_ffn": [_P] * 6 + [_I] * 5 + [_P],
+    "blockwise_ffn_bwd": [_P] * 10 + [_I] * 5 + [_P],
+    "blockwise_linear": [_P] * 4 + [_I] * 4 + [_P],
+    "blockwise_linear_bwd": [_P] * 5 + [_I] * 4 + [_P],
+}
+
+
+class RingAttnError(RuntimeError):
+    """A library call returned a non-zero ra_status."""
+
+    def __init__(self, name, code, msg):
+        super().__init__("%s failed (status %d): %s" % (name, code, msg))
+        self.code = code
+
+
+def library_path():
+    return os.path.join(_HERE, "libringattn.so")
+
+
+def load():
+    """Load the shared library (once).  Raises if it is missing."""
+    global _LIB
+    if _LIB is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError("%s is not built; run __graft_entry__.build() or "
+                               "python -m paper_2310_01889_amd.build" % path)
+        lib = ctypes.CDLL(path)
+        for name, args in _SIGS.items():
+            fn = getattr(lib, name, None)
+            if fn is None:  # checked by the symbol test; calling it raises AttributeError
+                continue
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        lib.ring_attn_last_error.argtypes = []
+        lib.ring_attn_last_error.restype = ctypes.c_char_p
+        _LIB = lib
+    return _LIB
+
+
+def exported_symbols():
+    """Names of the C entry points the binding expects the library to export."""
+    return sorted(list(_SIGS) + ["ring_attn_last_error"])
+
+
+def _call(name, *args):
+    lib = load()
+    rc = getattr(lib, name)(*args)
+    if rc != 0:
+        raise RingAttnError(name, rc, lib.ring_attn_last_error().decode())
+
+
+def _ptr(t, dtype=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _bshd(q):
+    if q.dim() != 4:
+        raise ValueError("expected a [B, S, H, D] tensor")
+    return tuple(int(x) for x in q.shape)
+
+
+# ----------------------------------------------------------------------------------
+# C entry points (outputs passed in)
+# ----------------------------------------------------------------------------------
+def ring_attn_fwd(q, k, v, o, lse, n_hosts, causal, stream=None):
+    B, S, H, D = _bshd(q)
+    bf = torch.bfloat16
+    _call("ring_attn_fwd", _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(o, bf, "o"),
+          _ptr(lse, torch.float32, "lse"), B, H, S, D, int(n_hosts), int(causal), _stream(stream))
+
+
+def ring_attn_fwd_f32(q, k, v, o, lse, n_hosts, causal, stream=None):
+    B, S, H, D = _bshd(q)
+    f = torch.float32
+    _call("ring_attn_fwd_f32", _ptr(q, f, "q"), _ptr(k, f, "k"), _ptr(v, f, "v"), _ptr(o, f, "o"),
+          _ptr(lse, f, "lse"), B, H, S, D, int(n_hosts), int(causal), _stream(stream))
+
+
+def ring_attn_bwd(q, k, v, o, lse, dO, dq, dk, dv, n_hosts, causal, stream=None):
+    B, S, H, D = _bshd(q)
+    bf = torch.bfloat16
+    _call("ring_attn_bwd", _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(o, bf, "o"),
+          _ptr(lse, torch.float32, "lse"), _ptr(dO, bf, "dO"), _ptr(dq, bf, "dq"), _ptr(dk, bf, "dk"),
+          _ptr(dv, bf, "dv"), B, H, S, D, int(n_hosts), int(causal), _stream(stream))
+
+
+def ring_attn_bwd_f32(q, k, v, o, lse, dO, dq, dk, dv, n_hosts, causal, stream=None):
+    B, S, H, D = _bshd(q)
+    f = torch.float32
+    _call("ring_attn_bwd_f32", _ptr(q, f, "q"), _ptr(k, f, "k"), _ptr(v, f, "v"), _ptr(o, f, "o"),
+          _ptr(lse, f, "lse"), _ptr(dO, f, "dO"), _ptr(dq, f, "dq"), _ptr(dk, f, "dk"), _ptr(dv, f, "dv"),
+          B, H, S, D, int(n_hosts), int(causal), _stream(stream))
+
+
+def ring_attn_fwd_host(q_blk, k_all, v_all, o_blk, lse_blk, n_hosts, host_idx, causal, stream=None):
+    B, c, H, D = _bshd(q_blk)
+    S = int(k_all.shape[1])
+    bf = torch.bfloat16
+    _call("ring_attn_fwd_host", _ptr(q_blk, bf, "q_blk"), _ptr(k_all, bf, "k_all"), _ptr(v_all, bf, "v_all"),
+          _ptr(o_blk, bf, "o_blk"), _ptr(lse_blk, torch.float32, "lse_blk"), B, H, S, D, int(n_hosts),
+          int(host_idx), int(causal), _stream(stream))
+
+
+def ring_attn_fwd_ordered(q, k, v, o, lse, n_hosts, causal, kv_order, stream=None):
+    B, S, H, D = _bshd(q)
+    bf = torch.bfloat16
+    flat = [int(x) for row in kv_order for x in row]
+    arr = (ctypes.c_int * len(flat))(*flat)
+    _call("ring_attn_fwd_ordered", _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(o, bf, "o"),
+          _ptr(lse, torch.float32, "lse"), B, H, S, D, int(n_hosts), int(causal),
+          ctypes.cast(arr, ctypes.c_void_p), _stream(stream))
+
+
+def blockwise_ffn(x, w1, b1, w2, b2, y, block, act=ACT_GELU_ERF, stream=None):
+    T, dm = (int(s) for s in x.shape)
+    dff = int(w1.shape[1])
+    bf = torch.bfloat16
+    _call("blockwise_ffn", _ptr(x, bf, "x"), _ptr(w1, bf, "w1"), _ptr(b1, bf, "b1"), _ptr(w2, bf, "w2"),
+          _ptr(b2, bf, "b2"), _ptr(y, bf, "y"), T, dm, dff, int(block), int(act), _stream(stream))
+
+
+def blockwise_ffn_bwd(x, w1, b1, w2, dy, dx, dw1, db1, dw2, db2, block, act=ACT_GELU_ERF, stream=None):
+    T, dm = (int(s) for s in x.shape)
+    dff = int(w1.shape[1])
+    bf, f = torch.bfloat16, torch.float32
+    _call("blockwise_ffn_bwd", _ptr(x, bf, "x"), _ptr(w1, bf, "w1"), _ptr(b1, bf, "b1"), _ptr(w2, bf, "w2"),
+          _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"), _ptr(dw1, f, "dw1"), _ptr(db1, f, "db1"), _ptr(dw2, f, "dw2"),
+          _ptr(db2, f, "db2"), T, dm, dff, int(block), int(act), _stream(stream))
+
+
+def blockwise_linear(x, w, residual, y, block, stream=None):
+    T, di = (int(s) for s in x.shape)
+    do = int(w.shape[1])
+    bf = torch.bfloat16
+    _call("blockwise_linear", _ptr(x, bf, "x"), _ptr(w, bf, "w"), _ptr(residual, bf, "residual"),
+          _ptr(y, bf, "y"), T, di, do, int(block), _stream(stream))
+
+
+def blockwise_linear_bwd(x, w, dy, dx, dw, block, stream=None):
+    T, di = (int(s) for s in x.shape)
+    do = int(w.shape[1])
+    bf = torch.bfloat16
+    _call("blockwise_linear_bwd", _ptr(x, bf, "x"), _ptr(w, bf, "w"), _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"),
+          _ptr(dw, torch.float32, "dw"), T, di, do, int(block), _stream(stream))
+
+
+# ----------------------------------------------------------------------------------
+# Allocating wrappers
+# ----------------------------------------------------------------------------------
+def attention_fwd(q, k, v, n_hosts, causal=True):
+    """Returns (o, lse) for bf16 or float32 q, k, v of shape [B, S, H, D]."""
+    B, S, H, D = _bshd(q)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, S), dtype=torch.float32, device=q.device)
+    fn = ring_attn_fwd if q.dtype == torch.bfloat16 else ring_attn_fwd_f32
+    fn(q, k, v, o, lse, n_hosts, causal)
+    return o, lse
+
+
+def attention_bwd(q, k, v, o, lse, dO, n_hosts, causal=True):
+    """Returns (dq, dk, dv)."""
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    fn = ring_attn_bwd if q.dtype == torch.bfloat16 else ring_attn_bwd_f32
+    fn(q, k, v, o, lse, dO, dq, dk, dv, n_hosts, causal)
+    return dq, dk, dv

@@ -1,0 +1,341 @@
+// Ring-attention forward step kernels for gfx950.
+//
+// One launch folds, for every host listed in the step, the key/value block that host
+// holds into its running state -- running row maximum m, running denominator l and
+// unnormalised output (numerator) acc -- as the online-softmax recurrence of the
+// paper's blockwise attention (Section 2 "Blockwise Parallel Transformers"; Section 3;
+// the carry of the Appendix A forward scan):
+//     m' = max(m, rowmax(s)),  p = exp(s - m'),
+//     l' = l * exp(m - m') + rowsum(p),  acc' = acc * exp(m - m') + p v
+// with s = q k^T / sqrt(D), masked (causal, by global position) keys giving p = 0.
+// On a host's first active step the state starts from (m=-inf, l=0, acc=0) in
+// registers; on its last it is finalised into o = acc / l and lse = m + ln l.
+#include "ra_common.h"
+#include "ra_kernels.h"
+
+namespace ra {
+
+// ===================================================================================
+// bf16 kernel: 4 waves, 128 queries per workgroup (32 per wave), 64-key tiles.
+//
+// Per wave, scores are formed transposed, S^T = K Q^T (32x32x16 MFMA, A = K rows from
+// LDS, B = Q held in registers), so that each lane owns one query: its row max and
+// row sum are in-lane reductions plus one exchange with lane l^32.  K rows are loaded
+// with bits 2 and 3 of the row index swapped, which makes each lane half hold 8
+// consecutive keys per 16-key group; the probabilities P^T then serve directly as the
+// B operand of O^T += V^T P^T, whose A operand is read from the row-major V tile with
+// the LDS transpose read.  O^T (128 dims x 32 queries per wave) stays in registers.
+// ===================================================================================
+namespace {
+
+constexpr int kBM = 128, kBN = 64, kThreads = 256;
+
+__device__ __forceinline__ int swap_bits23(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) {
+  constexpr int KS = D + 8;    // LDS row stride of the K tile (elements)
+  constexpr int VS = D + 32;   // LDS row stride of the V tile (elements)
+  constexpr int NKK = D / 16;  // 16-wide reduction steps of q.k
+  constexpr int NDT = D / 32;  // 32-row output tiles of O^T
+  constexpr int CPR = D / 8;                  // 16-byte chunks per row
+  constexpr int RPP = kThreads / CPR;         // rows per staging pass
+  constexpr int NPASS = kBN / RPP;            // staging passes per tile
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][kBN * KS];
+  __shared__ __attribute__((aligned(16))) bf16 sV[2][kBN * VS];
+
+  const int n_qt = p.c / kBM;
+  const int BH = p.B * p.H;
+  const int total = p.n_slots * BH * n_qt;
+  const int L = xcd_swizzle(blockIdx.x, total);
+  const int grp = L / n_qt;
+  const int qt = n_qt - 1 - (L % n_qt);  // longest causal rows first
+  const int slot = grp / BH, bh = grp % BH;
+  const int b = bh / p.H, h = bh % p.H;
+  const StepHost hs = p.host[slot];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, hi = lane >> 5;
+  const int rs = p.H * D;  // row stride of q / k / v / o (elements)
+
+  const int q_tile_row = hs.q_row0 + qt * kBM;       // first q-space row of the workgroup
+  const int qr = q_tile_row + wave * 32 + l32;       // this lane's query row
+  const int qpos = hs.q_pos0 + qt * kBM + wave * 32 + l32;
+  const int tile_first_q = hs.q_pos0 + qt * kBM;
+
+  const bf16* qbase = (const bf16*)p.q + (long long)b * p.q_bstride + h * D;
+  const bf16* kbase = (const bf16*)hs.k + (long long)b * hs.kv_bstride + h * D;
+  const bf16* vbase = (const bf16*)hs.v + (long long)b * hs.kv_bstride + h * D;
+
+  // number of key tiles with at least one visible key for this workgroup
+  int nt = p.c / kBN;
+  if (p.causal) {
+    const int vis = tile_first_q + kBM - hs.k_pos0;  // keys visible to the last row
+    nt = min(nt, max(0, (vis + kBN - 1) / kBN));
+  }
+
+  // ---- running state -------------------------------------------------------------
+  f32x16 oacc[NDT];
+  float m_run, l_run;
+  const long long st_row = (long long)bh * p.Sq + qr;
+  float* acc_tile = p.acc + ((long long)bh * (p.Sq / kBM) + q_tile_row / kBM) * (kBM * D);
+  if (hs.flags & kFirst) {
+    for (int dt = 0; dt < NDT; ++dt)
+      for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
+    m_run = -INFINITY;
+    l_run = 0.f;
+  } else {
+    for (int dt = 0; dt < NDT; ++dt)
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 t = ((const f32x4*)acc_tile)[((wave * NDT + dt) * 4 + g) * 64 + lane];
+        for (int e = 0; e < 4; ++e) oacc[dt][4 * g + e] = t[e];
+      }
+    m_run = p.m[st_row];
+    l_run = hi ? 0.f : p.l[st_row];
+  }
+
+  // ---- Q in registers: B operand of S^T = K Q^T (n = query, k = dim) ---------------
+  bf16x8 qreg[NKK];
+  {
+    const bf16* qrow = qbase + (long long)qr * rs;
+    for (int kk = 0; kk < NKK; ++kk) qreg[kk] = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
+  }
+
+  // ---- staging helpers ---------------------------------------------------------------
+  const int st_row_in_pass = tid / CPR, st_col = (tid % CPR) * 8;
+  u32x4 kpre[NPASS], vpre[NPASS];
+  auto gload = [&](int it) {
+    const int r0 = it * kBN + st_row_in_pass;
+    for (int ps = 0; ps < NPASS; ++ps) {
+      const long long off = (long long)(r0 + ps * RPP) * rs + st_col;
+      kpre[ps] = *(const u32x4*)(kbase + off);
+      vpre[ps] = *(const u32x4*)(vbase + off);
+    }
+  };
+  auto lstore = [&](int buf) {
+    for (int ps = 0; ps < NPASS; ++ps) {
+      const int r = st_row_in_pass + ps * RPP;
+      *(u32x4*)(&sK[buf][r * KS + st_col]) = kpre[ps];
+      *(u32x4*)(&sV[buf][r * VS + st_col]) = vpre[ps];
+    }
+  };
+
+  const float sl2 = p.scale * kLog2e;
+  const int krow_perm = swap_bits23(l32);
+
+  if (nt > 0) {
+    gload(0);
+    lstore(0);
+  }
+  __syncthreads();
+
+  for (int it = 0; it < nt; ++it) {
+    const int buf = it & 1;
+    if (it + 1 < nt) gload(it + 1);
+
+    // S^T = K Q^T for 64 keys x 32 queries: two 32-key tiles
+    f32x16 sacc[2];
+    for (int mt = 0; mt < 2; ++mt) {
+      for (int i = 0; i < 16; ++i) sacc[mt][i] = 0.f;
+      const bf16* krow = &sK[buf][(32 * mt + krow_perm) * KS + 8 * hi];
+      for (int kk = 0; kk < NKK; ++kk)
+        sacc[mt] = mfma32(*(const bf16x8*)(krow + 16 * kk), qreg[kk], sacc[mt]);
+    }
+
+    // causal mask: only tiles whose last key lies after the workgroup's first query
+    const int kpos0 = hs.k_pos0 + it * kBN;
+    if (p.causal && kpos0 + kBN - 1 > tile_first_q) {
+      for (int mt = 0; mt < 2; ++mt)
+        for (int i = 0; i < 16; ++i) {
+          const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
+          if (kpos > qpos) sacc[mt][i] = -INFINITY;
+        }
+    }
+
+    // online softmax (log2 domain): each lane owns one query, the partner lane l^32
+    // holds the other half of its keys
+    float mx = -INFINITY;
+    for (int mt = 0; mt < 2; ++mt)
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[mt][i]);
+    mx = pair_max(mx);
+    const float m_new = fmaxf(m_run, mx * sl2);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = fast_exp2(m_run - m_use);
+    m_run = m_new;
+    float rsum = 0.f;
+    bf16x8 pb[4];
+    for (int kb = 0; kb < 4; ++kb) {
+      uint32_t w[4];
+      for (int j = 0; j < 4; ++j) {
+        const float p0 = fast_exp2(fmaf(sacc[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
+        const float p1 = fast_exp2(fmaf(sacc[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
+        rsum += p0 + p1;
+        w[j] = pack_bf16x2(p0, p1);
+      }
+      u32x4 wv = {w[0], w[1], w[2], w[3]};
+      pb[kb] = __builtin_bit_cast(bf16x8, wv);
+    }
+    l_run = l_run * alpha + rsum;
+    for (int dt = 0; dt < NDT; ++dt)
+      for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
+
+    // O^T += V^T P^T: A operand = V^T (m = dim, k = key) via LDS transpose reads
+    {
+      const int g = lane >> 4, li = lane & 15;
+      const int dcol = 16 * (g & 1) + 4 * (li & 3);
+      const int krow = 8 * hi + (li >> 2);
+      for (int kb = 0; kb < 4; ++kb) {
+        const bf16* vp = &sV[buf][(16 * kb + krow) * VS + dcol];
+        for (int dt = 0; dt < NDT; ++dt) {
+          const bf16x4 lo = lds_read_tr16(vp + 32 * dt);
+          const bf16x4 up = lds_read_tr16(vp + 4 * VS + 32 * dt);
+          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+          oacc[dt] = mfma32(a, pb[kb], oacc[dt]);
+        }
+      }
+    }
+
+    if (it + 1 < nt) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- end of step: finalise or save the running state -------------------------------
+  const float l_tot = pair_sum(l_run);
+  if (hs.flags & kLast) {
+    const float inv = 1.f / l_tot;
+    bf16* orow = (bf16*)p.o + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+    for (int dt = 0; dt < NDT; ++dt)
+      for (int g = 0; g < 4; ++g) {
+        const int d = 32 * dt + 8 * g + 4 * hi;
+        u32x2 w = {pack_bf16x2(oacc[dt][4 * g] * inv, oacc[dt][4 * g + 1] * inv),
+                   pack_bf16x2(oacc[dt][4 * g + 2] * inv, oacc[dt][4 * g + 3] * inv)};
+        *(u32x2*)(orow + d) = w;
+      }
+    if (!hi) p.lse[st_row] = m_run * kLn2 + logf(l_tot);
+  } else {
+    for (int dt = 0; dt < NDT; ++dt)
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 t = {oacc[dt][4 * g], oacc[dt][4 * g + 1], oacc[dt][4 * g + 2], oacc[dt][4 * g + 3]};
+        ((f32x4*)acc_tile)[((wave * NDT + dt) * 4 + g) * 64 + lane] = t;
+      }
+    if (!hi) {
+      p.m[st_row] = m_run;
+      p.l[st_row] = l_tot;
+    }
+  }
+}
+
+// ===================================================================================
+// float32 kernel (exact float32 arithmetic, no matrix cores): one thread per query,
+// 64 queries per workgroup, 32-key tiles staged in LDS.  Natural-log state.
+// ===================================================================================
+constexpr int kF32BM = 64, kF32BN = 32;
+
+template <int D>
+__global__ __launch_bounds__(64) void fwd_f32_kernel(const FwdStep p) {
+  __shared__ float sK[kF32BN * D];
+  __shared__ float sV[kF32BN * D];
+  const int n_qt = p.c / kF32BM;
+  const int BH = p.B * p.H;
+  const int total = p.n_slots * BH * n_qt;
+  const int L = blockIdx.x;
+  if (L >= total) return;
+  const int grp = L / n_qt, qt = L % n_qt;
+  const int slot = grp / BH, bh = grp % BH;
+  const int b = bh / p.H, h = bh % p.H;
+  const StepHost hs = p.host[slot];
+  const int t = threadIdx.x;
+  const int rs = p.H * D;
+  const int qr = hs.q_row0 + qt * kF32BM + t;
+  const int qpos = hs.q_pos0 + qt * kF32BM + t;
+  const long long st_row = (long long)bh * p.Sq + qr;
+
+  const float* qrow = (const float*)p.q + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+  const float* kbase = (const float*)hs.k + (long long)b * hs.kv_bstride + h * D;
+  const float* vbase = (const float*)hs.v + (long long)b * hs.kv_bstride + h * D;
+  float* accrow = p.acc + st_row * D;
+
+  float q[D], acc[D];
+  for (int d = 0; d < D; ++d) q[d] = qrow[d];
+  float m_run, l_run;
+  if (hs.flags & kFirst) {
+    for (int d = 0; d < D; ++d) acc[d] = 0.f;
+    m_run = -INFINITY;
+    l_run = 0.f;
+  } else {
+    for (int d = 0; d < D; ++d) acc[d] = accrow[d];
+    m_run = p.m[st_row];
+    l_run = p.l[st_row];
+  }
+
+  int nt = p.c / kF32BN;
+  if (p.causal) {
+    const int vis = hs.q_pos0 + qt * kF32BM + kF32BM - hs.k_pos0;
+    nt = min(nt, max(0, (vis + kF32BN - 1) / kF32BN));
+  }
+  for (int it = 0; it < nt; ++it) {
+    __syncthreads();
+    for (int e = t; e < kF32BN * D; e += 64) {
+      const int r = e / D, d = e % D;
+      const long long off = (long long)(it * kF32BN + r) * rs + d;
+      sK[e] = kbase[off];
+      sV[e] = vbase[off];
+    }
+    __syncthreads();
+    float s[kF32BN];
+    float mx = -INFINITY;
+    for (int j = 0; j < kF32BN; ++j) {
+      float dot = 0.f;
+      for (int d = 0; d < D; ++d) dot = fmaf(q[d], sK[j * D + d], dot);
+      const int kpos = hs.k_pos0 + it * kF32BN + j;
+      s[j] = (p.causal && kpos > qpos) ? -INFINITY : dot * p.scale;
+      mx = fmaxf(mx, s[j]);
+    }
+    const float m_new = fmaxf(m_run, mx);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = expf(m_run - m_use);
+    m_run = m_new;
+    l_run *= alpha;
+    for (int d = 0; d < D; ++d) acc[d] *= alpha;
+    for (int j = 0; j < kF32BN; ++j) {
+      const float pj = expf(s[j] - m_use);
+      l_run += pj;
+      for (int d = 0; d < D; ++d) acc[d] = fmaf(pj, sV[j * D + d], acc[d]);
+    }
+  }
+  if (hs.flags & kLast) {
+    float* orow = (float*)p.o + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+    for (int d = 0; d < D; ++d) orow[d] = acc[d] / l_run;
+    p.lse[st_row] = m_run + logf(l_run);
+  } else {
+    for (int d = 0; d < D; ++d) accrow[d] = acc[d];
+    p.m[st_row] = m_run;
+    p.l[st_row] = l_run;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_fwd_bf16(const FwdStep& s, int D, hipStream_t st) {
+  const int total = s.n_slots * s.B * s.H * (s.c / kBM);
+  if (total == 0) return hipSuccess;
+  if (D == 128)
+    hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(total), dim3(kThreads), 0, st, s);
+  else
+    hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(total), dim3(kThreads), 0, st, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd_f32(const FwdStep& s, int D, hipStream_t st) {
+  const int total = s.n_slots * s.B * s.H * (s.c / kF32BM);
+  if (total == 0) return hipSuccess;
+  if (D == 128)
+    hipLaunchKernelGGL(fwd_f32_kernel<128>, dim3(total), dim3(64), 0, st, s);
+  else
+    hipLaunchKernelGGL(fwd_f32_kernel<64>, dim3(total), dim3(64), 0, st, s);
+  return hipGetLastError();
+}
+
+}  // namespace ra

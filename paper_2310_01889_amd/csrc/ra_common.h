@@ -1,0 +1,79 @@
+// Internal helpers shared by the gfx950 kernels and the host scheduler.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ra {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// ---------------------------------------------------------------------------------
+// Matrix-core helpers (gfx950).  Lane layouts, verified on the device:
+//   32x32x16 bf16:  A[m][k]: lane l holds m = l%32, k = 8*(l/32) + 0..7
+//                   B[k][n]: lane l holds n = l%32, k = 8*(l/32) + 0..7
+//                   C[m][n]: lane l, reg i holds n = l%32, m = 8*(i/4) + 4*(l/32) + i%4
+//   16x16x32 bf16:  A: m = l%16, k = 8*(l/16) + 0..7;  B: n = l%16, same k;
+//                   C: reg i holds n = l%16, m = 4*(l/16) + i
+// Any permutation of k applied to both operands leaves the product unchanged.
+// ---------------------------------------------------------------------------------
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// LDS transpose read (ds_read_b64_tr_b16).  Within each group of 16 lanes, lane L
+// supplies the address of 4 consecutive 16-bit values M[L][0..3]; lane i receives
+// element j = M[4j + i/4][i%4].  Used to feed a row-major [k][n] tile as an operand
+// whose lanes run along n and registers along k.
+__device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* lds_ptr) {
+  s16x4 t = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)((lds_void*)lds_ptr));
+  return __builtin_bit_cast(bf16x4, t);
+}
+
+// Max / sum of a value with the same value in lane l ^ 32 (v_permlane32_swap).
+__device__ __forceinline__ float pair_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Two float -> packed bf16 pair, round-to-nearest-even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Map a linear workgroup id so that each XCD (workgroups are dispatched round-robin
+// over the 8 XCDs) receives a contiguous range of logical tiles: tiles that share
+// key/value data then share one L2.
+__device__ __forceinline__ int xcd_swizzle(int id, int total) {
+  const int nx = 8;
+  const int per = total / nx, rem = total % nx;
+  const int xcd = id % nx, n = id / nx;
+  return xcd * per + (xcd < rem ? xcd : rem) + n;
+}
+
+}  // namespace ra

@@ -1,0 +1,457 @@
+// Virtual-ring scheduler and the C ABI of the attention entry points.
+//
+// The ring of Section 3 is emulated on one device.  Every host's query block and every
+// key/value block live in device memory.  A call runs n_hosts steps; at step t, host i
+// folds in key/value block order(i, t) -- (i - t) mod n_hosts for the ring -- and every
+// host with work at that step is one slot of a single kernel launch.  Step 0 reads each
+// host's block where it lies (a host's own block needs no transfer).  For t >= 1 the
+// block comes from that host's receive buffer: two slots used alternately (the
+// double buffer of the paper's memory accounting: current and receiving key/value
+// blocks).  The copies that fill the slot for step t+1 run on a library-owned side
+// stream while step t computes (the ppermute of the paper's code, overlapped with the
+// blockwise computation); events order every copy after the last reader of its slot
+// and every step after its copy.
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "ra_common.h"
+#include "ra_kernels.h"
+#include "ringattn.h"
+
+namespace ra {
+
+thread_local std::string g_err;
+
+int set_err(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define RA_HIP(expr)                                                                   \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return set_err(e_ == hipErrorOutOfMemory ? RA_ENOMEM : RA_EHIP, "%s failed: %s", \
+                     #expr, hipGetErrorString(e_));                                    \
+  } while (0)
+
+// ---------------------------------------------------------------------------------
+// Per-device side stream (created once, default priority) and memory-pool setting.
+// ---------------------------------------------------------------------------------
+namespace {
+std::mutex g_mu;
+hipStream_t g_side[64];
+}  // namespace
+
+int side_stream(hipStream_t* out) {
+  int dev = 0;
+  RA_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return set_err(RA_EHIP, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_side[dev]) {
+    RA_HIP(hipStreamCreateWithFlags(&g_side[dev], hipStreamNonBlocking));
+    // keep stream-ordered allocations cached in the pool between calls
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+      uint64_t thr = ~0ull;
+      (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+    }
+  }
+  *out = g_side[dev];
+  return RA_OK;
+}
+
+static bool env_flag(const char* name) {
+  const char* v = getenv(name);
+  return v && v[0] && v[0] != '0';
+}
+
+// Stream-ordered workspace and events owned by one call; released on every exit path.
+struct CallResources {
+  hipStream_t stream;
+  void* ws = nullptr;
+  std::vector<hipEvent_t> events;
+  explicit CallResources(hipStream_t s) : stream(s) {}
+  ~CallResources() {
+    if (ws) (void)hipFreeAsync(ws, stream);
+    for (hipEvent_t e : events) (void)hipEventDestroy(e);
+  }
+  int alloc(size_t bytes) {
+    if (bytes == 0) return RA_OK;
+    RA_HIP(hipMallocAsync(&ws, bytes, stream));
+    return RA_OK;
+  }
+  int event(hipEvent_t* e) {
+    RA_HIP(hipEventCreateWithFlags(e, hipEventDisableTiming));
+    events.push_back(*e);
+    return RA_OK;
+  }
+};
+
+// ---------------------------------------------------------------------------------
+// Ring plan shared by forward and backward.
+// ---------------------------------------------------------------------------------
+struct RingProblem {
+  const void *q, *k, *v;
+  int B, H, S, D, N, causal, elt;   // elt: bytes per element (2 = bf16, 4 = float32)
+  int Sq;                           // rows of q / o / lse: S (all hosts) or c (one host)
+  std::vector<int> hosts;           // hosts evaluated by this call
+  std::vector<int> order;           // order[i * N + t] (empty: ring order (i - t) mod N)
+  int c() const { return S / N; }
+  int blk(int i, int t) const { return order.empty() ? ((i - t) % N + N) % N : order[i * N + t]; }
+  bool active(int i, int j) const { return !causal || j <= i; }  // block j not fully masked
+  int q_row0(int i) const { return Sq == S ? i * c() : 0; }
+};
+
+// Receive buffers: slot s (0/1) of host-slot hslot, for k and v.
+struct RecvBuffers {
+  char* base = nullptr;
+  size_t blk_bytes = 0;
+  int nh = 0;
+  char* k(int s, int hslot) const { return base + ((size_t)(s * nh + hslot)) * blk_bytes; }
+  char* v(int s, int hslot) const { return base + ((size_t)((2 + s) * nh + hslot)) * blk_bytes; }
+  static size_t bytes(size_t blk_bytes, int nh) { return 4 * (size_t)nh * blk_bytes; }
+};
+
+static int copy_block(const RingProblem& P, const void* src_all, char* dst, int j, hipStream_t st) {
+  const size_t rowb = (size_t)P.H * P.D * P.elt;
+  const size_t blkb = (size_t)P.c() * rowb;
+  const char* src = (const char*)src_all + (size_t)j * blkb;
+  if (P.B == 1) {
+    RA_HIP(hipMemcpyAsync(dst, src, blkb, hipMemcpyDeviceToDevice, st));
+  } else {
+    RA_HIP(hipMemcpy2DAsync(dst, blkb, src, (size_t)P.S * rowb, blkb, P.B, hipMemcpyDeviceToDevice, st));
+  }
+  return RA_OK;
+}
+
+// Enqueue the whole ring: `launch(t, hosts_of_step)` is called once per step with, for
+// every active host, (host, block, kv pointers, batch stride, first/last flags).
+template <class Launch>
+static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, char* recv_base,
+                    Launch&& launch) {
+  const int N = P.N;
+  const int nh = (int)P.hosts.size();
+  RecvBuffers rb;
+  rb.base = recv_base;
+  rb.blk_bytes = (size_t)P.B * P.c() * P.H * P.D * P.elt;
+  rb.nh = nh;
+
+  // first / last active step of every host
+  std::vector<int> first(nh, -1), last(nh, -1);
+  for (int t = 0; t < N; ++t)
+    for (int s = 0; s < nh; ++s)
+      if (P.active(P.hosts[s], P.blk(P.hosts[s], t))) {
+        if (first[s] < 0) first[s] = t;
+        last[s] = t;
+      }
+
+  const bool serial = env_flag("RINGATTN_SERIAL_COPY");
+  const bool poison = env_flag("RINGATTN_POISON");
+  hipStream_t side = stream;
+  if (!serial && N > 1) {
+    int rc = side_stream(&side);
+    if (rc) return rc;
+  }
+  std::vector<hipEvent_t> ev_copy(N + 1, nullptr);
+  hipEvent_t ev_entry = nullptr;
+  if (side != stream) {
+    int rc = R.event(&ev_entry);
+    if (rc) return rc;
+    RA_HIP(hipEventRecord(ev_entry, stream));
+    RA_HIP(hipStreamWaitEvent(side, ev_entry, 0));
+  }
+  auto enqueue_copies = [&](int t) -> int {
+    for (int s = 0; s < nh; ++s) {
+      const int i = P.hosts[s], j = P.blk(i, t);
+      if (!P.active(i, j)) continue;
+      if (poison) {  // a step that read its slot before this copy landed would see NaN
+        RA_HIP(hipMemsetAsync(rb.k(t & 1, s), 0xFF, rb.blk_bytes, side));
+        RA_HIP(hipMemsetAsync(rb.v(t & 1, s), 0xFF, rb.blk_bytes, side));
+      }
+      int rc = copy_block(P, P.k, rb.k(t & 1, s), j, side);
+      if (!rc) rc = copy_block(P, P.v, rb.v(t & 1, s), j, side);
+      if (rc) return rc;
+    }
+    if (side != stream) {
+      int rc = R.event(&ev_copy[t]);
+      if (rc) return rc;
+      RA_HIP(hipEventRecord(ev_copy[t], side));
+    }
+    return RA_OK;
+  };
+  if (N > 1 && !serial) {
+    int rc = enqueue_copies(1);
+    if (!rc && N > 2) rc = enqueue_copies(2);
+    if (rc) return rc;
+  }
+
+  const size_t rowe = (size_t)P.H * P.D;
+  for (int t = 0; t < N; ++t) {
+    if (t >= 1) {
+      if (serial) {
+        int rc = enqueue_copies(t);
+        if (rc) return rc;
+      } else {
+        RA_HIP(hipStreamWaitEvent(stream, ev_copy[t], 0));
+      }
+    }
+    std::vector<StepHost> hs;
+    std::vector<int> host_ids, blk_ids;
+    for (int s = 0; s < nh; ++s) {
+      const int i = P.hosts[s], j = P.blk(i, t);
+      if (!P.active(i, j)) continue;
+      StepHost h{};
+      if (t == 0) {
+        h.k = (const char*)P.k + (size_t)j * P.c() * rowe * P.elt;
+        h.v = (const char*)P.v + (size_t)j * P.c() * rowe * P.elt;
+        h.kv_bstride = (long long)P.S * rowe;
+      } else {
+        h.k = rb.k(t & 1, s);
+        h.v = rb.v(t & 1, s);
+        h.kv_bstride = (long long)P.c() * rowe;
+      }
+      h.q_row0 = P.q_row0(i);
+      h.q_pos0 = i * P.c();
+      h.k_pos0 = j * P.c();
+      h.flags = (t == first[s] ? kFirst : 0) | (t == last[s] ? kLast : 0);
+      hs.push_back(h);
+      host_ids.push_back(i);
+      blk_ids.push_back(j);
+    }
+    int rc = launch(t, hs, host_ids, blk_ids);
+    if (rc) return rc;
+    if (!serial && t >= 1 && t + 2 < N) {
+      hipEvent_t done;
+      rc = R.event(&done);
+      if (rc) return rc;
+      RA_HIP(hipEventRecord(done, stream));
+      RA_HIP(hipStreamWaitEvent(side, done, 0));
+      rc = enqueue_copies(t + 2);
+      if (rc) return rc;
+    }
+  }
+  if (side != stream) {
+    hipEvent_t tail;
+    int rc = R.event(&tail);
+    if (rc) return rc;
+    RA_HIP(hipEventRecord(tail, side));
+    RA_HIP(hipStreamWaitEvent(stream, tail, 0));
+  }
+  return RA_OK;
+}
+
+// ---------------------------------------------------------------------------------
+// Forward
+// ---------------------------------------------------------------------------------
+static int run_fwd(const RingProblem& P, void* o, float* lse, hipStream_t stream) {
+  const int nh = (int)P.hosts.size();
+  const size_t recv = P.N > 1 ? RecvBuffers::bytes((size_t)P.B * P.c() * P.H * P.D * P.elt, nh) : 0;
+  const size_t nrow = (size_t)P.B * P.H * P.Sq;
+  const bool need_state = P.N > 1;
+  const size_t state = need_state ? nrow * (P.D + 2) * sizeof(float) : 0;
+  CallResources R(stream);
+  int rc = R.alloc(recv + state);
+  if (rc) return rc;
+  char* base = (char*)R.ws;
+  float* acc = need_state ? (float*)(base + recv) : nullptr;
+  float* m = need_state ? acc + nrow * P.D : nullptr;
+  float* l = need_state ? m + nrow : nullptr;
+
+  FwdStep st{};
+  st.q = P.q;
+  st.o = o;
+  st.lse = lse;
+  st.acc = acc;
+  st.m = m;
+  st.l = l;
+  st.q_bstride = (long long)P.Sq * P.H * P.D;
+  st.B = P.B;
+  st.H = P.H;
+  st.Sq = P.Sq;
+  st.c = P.c();
+  st.causal = P.causal;
+  st.scale = 1.0f / sqrtf((float)P.D);
+  return run_ring(P, stream, R, base, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
+                                          const std::vector<int>&) -> int {
+    st.n_slots = (int)hs.size();
+    for (size_t s = 0; s < hs.size(); ++s) st.host[s] = hs[s];
+    RA_HIP(P.elt == 2 ? launch_fwd_bf16(st, P.D, stream) : launch_fwd_f32(st, P.D, stream));
+    return RA_OK;
+  });
+}
+
+// ---------------------------------------------------------------------------------
+// Backward
+// ---------------------------------------------------------------------------------
+static int run_bwd(const RingProblem& P, const void* o, const float* lse, const void* dO, void* dq,
+                   void* dk, void* dv, hipStream_t stream) {
+  const int nh = (int)P.hosts.size();
+  const size_t recv = P.N > 1 ? RecvBuffers::bytes((size_t)P.B * P.c() * P.H * P.D * P.elt, nh) : 0;
+  const size_t nrow = (size_t)P.B * P.H * P.Sq;
+  const size_t telems = (size_t)P.B * P.S * P.H * P.D;
+  const bool f32 = P.elt == 4;  // float32 gradients accumulate straight into the outputs
+  const size_t grads = f32 ? 0 : 3 * telems * sizeof(float);
+  CallResources R(stream);
+  int rc = R.alloc(recv + nrow * sizeof(float) + grads);
+  if (rc) return rc;
+  char* base = (char*)R.ws;
+  float* delta = (float*)(base + recv);
+  float* gq = f32 ? (float*)dq : delta + nrow;
+  float* gk = f32 ? (float*)dk : gq + telems;
+  float* gv = f32 ? (float*)dv : gk + telems;
+  RA_HIP(launch_zero_f32(gq, (long long)telems, stream));
+  RA_HIP(launch_zero_f32(gk, (long long)telems, stream));
+  RA_HIP(launch_zero_f32(gv, (long long)telems, stream));
+  if (f32)
+    RA_HIP(launch_bwd_pre_f32((const float*)o, (const float*)dO, delta, P.B, P.Sq, P.H, P.D, stream));
+  else
+    RA_HIP(launch_bwd_pre_bf16(o, dO, delta, P.B, P.Sq, P.H, P.D, stream));
+
+  BwdStep st{};
+  st.q = P.q;
+  st.dO = dO;
+  st.lse = lse;
+  st.delta = delta;
+  st.dq = gq;
+  st.dk = gk;
+  st.dv = gv;
+  st.q_bstride = (long long)P.Sq * P.H * P.D;
+  st.dkv_bstride = (long long)P.S * P.H * P.D;
+  st.B = P.B;
+  st.H = P.H;
+  st.Sq = P.Sq;
+  st.c = P.c();
+  st.causal = P.causal;
+  st.scale = 1.0f / sqrtf((float)P.D);
+  rc = run_ring(P, stream, R, base, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
+                                        const std::vector<int>& blks) -> int {
+    st.n_slots = (int)hs.size();
+    for (size_t s = 0; s < hs.size(); ++s) {
+      st.host[s] = hs[s];
+      st.dkv_row0[s] = blks[s] * P.c();
+    }
+    RA_HIP(f32 ? launch_bwd_f32(st, P.D, stream) : launch_bwd_bf16(st, P.D, stream));
+    return RA_OK;
+  });
+  if (rc) return rc;
+  if (!f32) {
+    RA_HIP(launch_cast_f32_bf16(gq, dq, (long long)telems, stream));
+    RA_HIP(launch_cast_f32_bf16(gk, dk, (long long)telems, stream));
+    RA_HIP(launch_cast_f32_bf16(gv, dv, (long long)telems, stream));
+  }
+  return RA_OK;
+}
+
+// ---------------------------------------------------------------------------------
+// Argument validation
+// ---------------------------------------------------------------------------------
+static int validate(int B, int H, int S, int D, int N, int causal, int tile) {
+  if (B <= 0 || H <= 0 || S <= 0 || D <= 0 || N <= 0)
+    return set_err(RA_EINVAL, "sizes must be positive (B=%d H=%d S=%d D=%d n_hosts=%d)", B, H, S, D, N);
+  if (causal != 0 && causal != 1) return set_err(RA_EINVAL, "causal must be 0 or 1 (got %d)", causal);
+  if (D != 64 && D != 128) return set_err(RA_EUNSUPPORTED, "head dim D=%d not supported (64 or 128)", D);
+  if (N > kMaxSlots) return set_err(RA_EUNSUPPORTED, "n_hosts=%d exceeds %d", N, kMaxSlots);
+  if (S % N) return set_err(RA_EUNSUPPORTED, "S=%d is not a multiple of n_hosts=%d", S, N);
+  if ((S / N) % tile)
+    return set_err(RA_EUNSUPPORTED, "block S/n_hosts=%d is not a multiple of %d", S / N, tile);
+  if ((long long)B * S * H * D >= (1ll << 31))
+    return set_err(RA_EUNSUPPORTED, "B*S*H*D = %lld elements exceeds 2^31-1", (long long)B * S * H * D);
+  return RA_OK;
+}
+
+static RingProblem all_hosts(const void* q, const void* k, const void* v, int B, int H, int S, int D, int N,
+                             int causal, int elt) {
+  RingProblem P{q, k, v, B, H, S, D, N, causal, elt, S, {}, {}};
+  for (int i = 0; i < N; ++i) P.hosts.push_back(i);
+  return P;
+}
+
+}  // namespace ra
+
+using namespace ra;
+
+extern "C" {
+
+const char* ring_attn_last_error(void) { return g_err.c_str(); }
+
+int ring_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S, int D,
+                  int n_hosts, int causal, hipStream_t stream) {
+  g_err.clear();
+  if (!q || !k || !v || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
+  int rc = validate(B, H, S, D, n_hosts, causal, 128);
+  if (rc) return rc;
+  return run_fwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 2), o, lse, stream);
+}
+
+int ring_attn_fwd_f32(const float* q, const float* k, const float* v, float* o, float* lse, int B, int H, int S,
+                      int D, int n_hosts, int causal, hipStream_t stream) {
+  g_err.clear();
+  if (!q || !k || !v || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
+  int rc = validate(B, H, S, D, n_hosts, causal, 64);
+  if (rc) return rc;
+  return run_fwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 4), o, lse, stream);
+}
+
+int ring_attn_fwd_host(const void* q_blk, const void* k_all, const void* v_all, void* o_blk, float* lse_blk, int B,
+                       int H, int S, int D, int n_hosts, int host_idx, int causal, hipStream_t stream) {
+  g_err.clear();
+  if (!q_blk || !k_all || !v_all || !o_blk || !lse_blk) return set_err(RA_EINVAL, "null pointer argument");
+  int rc = validate(B, H, S, D, n_hosts, causal, 128);
+  if (rc) return rc;
+  if (host_idx < 0 || host_idx >= n_hosts)
+    return set_err(RA_EINVAL, "host_idx=%d outside [0, n_hosts=%d)", host_idx, n_hosts);
+  RingProblem P{q_blk, k_all, v_all, B, H, S, D, n_hosts, causal, 2, S / n_hosts, {host_idx}, {}};
+  return run_fwd(P, o_blk, lse_blk, stream);
+}
+
+int ring_attn_fwd_ordered(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S,
+                          int D, int n_hosts, int causal, const int* kv_order, hipStream_t stream) {
+  g_err.clear();
+  if (!q || !k || !v || !o || !lse || !kv_order) return set_err(RA_EINVAL, "null pointer argument");
+  int rc = validate(B, H, S, D, n_hosts, causal, 128);
+  if (rc) return rc;
+  RingProblem P = all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 2);
+  P.order.assign(kv_order, kv_order + (size_t)n_hosts * n_hosts);
+  for (int i = 0; i < n_hosts; ++i) {
+    std::vector<int> seen(n_hosts, 0);
+    for (int t = 0; t < n_hosts; ++t) {
+      const int j = P.order[i * n_hosts + t];
+      if (j < 0 || j >= n_hosts || seen[j]++)
+        return set_err(RA_EINVAL, "kv_order row %d is not a permutation of 0..%d", i, n_hosts - 1);
+    }
+  }
+  return run_fwd(P, o, lse, stream);
+}
+
+int ring_attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse, const void* dO,
+                  void* dq, void* dk, void* dv, int B, int H, int S, int D, int n_hosts, int causal,
+                  hipStream_t stream) {
+  g_err.clear();
+  if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv) return set_err(RA_EINVAL, "null pointer argument");
+  int rc = validate(B, H, S, D, n_hosts, causal, 128);
+  if (rc) return rc;
+  return run_bwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 2), o, lse, dO, dq, dk, dv, stream);
+}
+
+int ring_attn_bwd_f32(const float* q, const float* k, const float* v, const float* o, const float* lse,
+                      const float* dO, float* dq, float* dk, float* dv, int B, int H, int S, int D, int n_hosts,
+                      int causal, hipStream_t stream) {
+  g_err.clear();
+  if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv) return set_err(RA_EINVAL, "null pointer argument");
+  int rc = validate(B, H, S, D, n_hosts, causal, 64);
+  if (rc) return rc;
+  return run_bwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 4), o, lse, dO, dq, dk, dv, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,191 @@
+"""GPU parity of the ring-attention entry points against the fp64 CPU oracle.
+
+Every case draws seeded inputs (paper_2310_01889_amd.synth), runs the HIP library through
+its C ABI, and compares element by element with oracle/ on the same values.
+Tolerances: float32 path max |err| <= 1e-5; bf16 path <= 2e-2 on o and lse, <= 5e-2 on
+dq, dk, dv (absolute, against the fp64 oracle).
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2310_01889_amd as ra
+from paper_2310_01889_amd import synth
+from oracle import attention as OA
+from oracle import ring as OR
+from tests.gpu_util import dev, log, max_err, np64
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-5
+TOL_O = 2e-2
+TOL_G = 5e-2
+
+
+def _fwd_case(seed, B, S, H, D, N, causal, dtype=torch.bfloat16):
+    log("fwd case seed=%d B=%d S=%d H=%d D=%d N=%d causal=%d %s" % (seed, B, S, H, D, N, causal, dtype))
+    q, k, v = synth.attention_inputs(seed, B, S, H, D, dtype)
+    o, lse = ra.attention_fwd(*dev(q, k, v), N, causal)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = OA.attention_fwd(np64(q), np64(k), np64(v), bool(causal))
+    return o, lse, o_ref, lse_ref, (q, k, v)
+
+
+def test_tiny_causal_fp32_config():
+    """B=1, H=1, S=1024, D=64, float32, ring of 4 hosts with 256-token blocks."""
+    o, lse, o_ref, lse_ref, _ = _fwd_case(1, 1, 1024, 1, 64, 4, 1, torch.float32)
+    assert max_err(o, o_ref) <= TOL_F32
+    assert max_err(lse, lse_ref) <= TOL_F32
+
+
+@pytest.mark.parametrize("N", [1, 2, 4])
+@pytest.mark.parametrize("causal", [0, 1])
+def test_fp32_forward_hosts(N, causal):
+    o, lse, o_ref, lse_ref, _ = _fwd_case(2, 2, 512, 3, 64, N, causal, torch.float32)
+    assert max_err(o, o_ref) <= TOL_F32
+    assert max_err(lse, lse_ref) <= TOL_F32
+
+
+def test_fp32_forward_d128():
+    o, lse, o_ref, lse_ref, _ = _fwd_case(3, 1, 256, 2, 128, 2, 1, torch.float32)
+    assert max_err(o, o_ref) <= TOL_F32
+    assert max_err(lse, lse_ref) <= TOL_F32
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("N", [1, 2, 4, 8])
+@pytest.mark.parametrize("causal", [0, 1])
+def test_bf16_forward_hosts(D, N, causal):
+    o, lse, o_ref, lse_ref, _ = _fwd_case(4, 2, 1024, 3, D, N, causal)
+    eo, el = max_err(o, o_ref), max_err(lse, lse_ref)
+    log("  max|o err| %.3e  max|lse err| %.3e" % (eo, el))
+    assert eo <= TOL_O and el <= TOL_O
+
+
+def test_bf16_forward_zero_query_prefix_mean_and_first_token():
+    """Q = 0: causal row r is the mean of V_0..V_r and lse = ln(r+1); row 0 is V_0 exactly."""
+    B, S, H, D = 1, 1024, 2, 128
+    _, k, v = synth.attention_inputs(5, B, S, H, D)
+    q = torch.zeros_like(v)
+    o, lse = ra.attention_fwd(*dev(q, k, v), 4, True)
+    torch.cuda.synchronize()
+    prefix = np.cumsum(np64(v), axis=1) / np.arange(1, S + 1)[None, :, None, None]
+    assert max_err(o, prefix) <= TOL_O
+    assert max_err(lse, np.broadcast_to(np.log(np.arange(1, S + 1)), (B, H, S))) <= TOL_O
+    assert torch.equal(o[:, 0].cpu(), v[:, 0])
+
+
+def test_bf16_forward_invariant_to_block_order():
+    B, S, H, D, N = 1, 1024, 2, 128, 4
+    q, k, v = synth.attention_inputs(6, B, S, H, D)
+    qd, kd, vd = dev(q, k, v)
+    o_ref, lse_ref = OA.attention_fwd(np64(q), np64(k), np64(v), True)
+    rng = np.random.default_rng(0)
+    orders = [[list(rng.permutation(N)) for _ in range(N)] for _ in range(3)]
+    orders.append([[(i - t) % N for t in range(N)] for i in range(N)])
+    for order in orders:
+        log("order %s" % order)
+        o = torch.empty_like(qd)
+        lse = torch.empty((B, H, S), dtype=torch.float32, device="cuda")
+        ra.ring_attn_fwd_ordered(qd, kd, vd, o, lse, N, True, order)
+        torch.cuda.synchronize()
+        assert max_err(o, o_ref) <= TOL_O
+        assert max_err(lse, lse_ref) <= TOL_O
+
+
+@pytest.mark.parametrize("host", [0, 3, 7])
+def test_bf16_one_host_share(host):
+    B, H, D, N, c = 1, 2, 128, 8, 256
+    S = N * c
+    q, k, v = synth.attention_inputs(7, B, S, H, D)
+    qb = q[:, host * c:(host + 1) * c].contiguous()
+    o = torch.empty(qb.shape, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((B, H, c), dtype=torch.float32, device="cuda")
+    ra.ring_attn_fwd_host(dev(qb), *dev(k, v), o, lse, N, host, True)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = OR.ring_host_fwd(np64(qb), np64(k), np64(v), N, host, True)
+    assert max_err(o, o_ref) <= TOL_O
+    assert max_err(lse, lse_ref) <= TOL_O
+
+
+@pytest.mark.parametrize("env", ["RINGATTN_SERIAL_COPY", "RINGATTN_POISON"])
+def test_bf16_copy_modes_match(env, monkeypatch):
+    """Receive buffers poisoned with NaN before every copy, or copies serialised on the
+    caller stream, give bit-identical results to the overlapped default."""
+    B, S, H, D, N = 1, 2048, 2, 128, 8
+    q, k, v = dev(*synth.attention_inputs(8, B, S, H, D))
+    o0, l0 = ra.attention_fwd(q, k, v, N, True)
+    monkeypatch.setenv(env, "1")
+    o1, l1 = ra.attention_fwd(q, k, v, N, True)
+    torch.cuda.synchronize()
+    assert torch.equal(o0, o1) and torch.equal(l0, l1)
+
+
+@pytest.mark.parametrize("N", [1, 2, 8])
+@pytest.mark.parametrize("causal", [0, 1])
+def test_bf16_backward(N, causal):
+    B, S, H, D = 1, 1024, 2, 128
+    log("bwd case N=%d causal=%d" % (N, causal))
+    q, k, v, do = synth.attention_inputs(9, B, S, H, D, with_grad=True)
+    qd, kd, vd, dod = dev(q, k, v, do)
+    o, lse = ra.attention_fwd(qd, kd, vd, N, causal)
+    dq, dk, dv = ra.attention_bwd(qd, kd, vd, o, lse, dod, N, causal)
+    torch.cuda.synchronize()
+    ref = OA.attention_bwd(np64(q), np64(k), np64(v), np64(do), bool(causal))
+    errs = [max_err(g, r) for g, r in zip((dq, dk, dv), ref)]
+    log("  max|dq,dk,dv err| %s" % errs)
+    assert max(errs) <= TOL_G
+
+
+def test_bf16_backward_d64_batch2():
+    B, S, H, D, N = 2, 512, 3, 64, 4
+    q, k, v, do = synth.attention_inputs(10, B, S, H, D, with_grad=True)
+    qd, kd, vd, dod = dev(q, k, v, do)
+    o, lse = ra.attention_fwd(qd, kd, vd, N, True)
+    grads = ra.attention_bwd(qd, kd, vd, o, lse, dod, N, True)
+    torch.cuda.synchronize()
+    ref = OA.attention_bwd(np64(q), np64(k), np64(v), np64(do), True)
+    assert max(max_err(g, r) for g, r in zip(grads, ref)) <= TOL_G
+
+
+def test_bf16_backward_gradient_invariants():
+    """sum_s dK_s = 0 and sum_s dV_s = sum_r dO_r for every (batch, head)."""
+    B, S, H, D, N = 1, 1024, 2, 128, 4
+    q, k, v, do = dev(*synth.attention_inputs(11, B, S, H, D, with_grad=True))
+    o, lse = ra.attention_fwd(q, k, v, N, True)
+    dq, dk, dv = ra.attention_bwd(q, k, v, o, lse, do, N, True)
+    torch.cuda.synchronize()
+    assert np.max(np.abs(np64(dk).sum(axis=1))) <= TOL_G * 8
+    assert np.max(np.abs(np64(dv).sum(axis=1) - np64(do).sum(axis=1))) <= TOL_G * 8
+    # first causal token: dQ_0 = 0
+    assert np.max(np.abs(np64(dq)[:, 0])) <= 1e-6
+
+
+@pytest.mark.parametrize("N", [1, 4])
+def test_fp32_backward(N):
+    B, S, H, D = 1, 256, 2, 64
+    q, k, v, do = synth.attention_inputs(12, B, S, H, D, torch.float32, with_grad=True)
+    qd, kd, vd, dod = dev(q, k, v, do)
+    o, lse = ra.attention_fwd(qd, kd, vd, N, True)
+    grads = ra.attention_bwd(qd, kd, vd, o, lse, dod, N, True)
+    torch.cuda.synchronize()
+    ref = OA.attention_bwd(np64(q), np64(k), np64(v), np64(do), True)
+    errs = [max_err(g, r) for g, r in zip(grads, ref)]
+    log("  fp32 bwd errs %s" % errs)
+    assert max(errs) <= TOL_F32
+
+
+def test_errors_leave_outputs_untouched():
+    q, k, v = dev(*synth.attention_inputs(13, 1, 512, 1, 128))
+    o = torch.full_like(q, 7.0)
+    lse = torch.full((1, 1, 512), 7.0, device="cuda")
+    with pytest.raises(ra.RingAttnError) as e:
+        ra.ring_attn_fwd(q, k, v, o, lse, 3, True)  # 512 % 3 != 0
+    assert e.value.code == 2
+    with pytest.raises(ra.RingAttnError) as e:
+        ra.ring_attn_fwd(q, k, v, o, lse, 8, True)  # block 64 is not a multiple of 128
+    assert e.value.code == 2
+    torch.cuda.synchronize()
+    assert bool((o == 7.0).all()) and bool((lse == 7.0).all())
