@@ -1,0 +1,180 @@
+#!/usr/bin/env python3
+"""Benchmark of the ring-attention hot path on one MI355X.
+
+Workload (one "step"): causal ring-attention forward, B=1, S=32768, H=32, D=128, bf16
+inputs N(0,1), ring of 8 virtual hosts with 4096-token blocks -- partition and ring
+schedule, key/value rotation through the double buffer on the side stream, the
+attention-step kernel on every host, and finalisation.  Inputs are resident in HBM before
+the timed region.  Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra]
+
+`value` is TFLOP/s of algorithmic work (4*B*H*D per visible (query, key) pair; causal
+masking halves the diagonal blocks and skips blocks above the diagonal).  The
+`roofline` object reports the step kernel's own throughput (HIP events around every
+launch, on the stream it runs on) against the bf16 dense matrix-core peak.  The
+`cpu_baseline` object times the fp64 CPU oracle on one head of the same workload and
+scales it to all 32 heads.  `extra` holds secondary configurations measured in the same
+run (forward+backward at S=16384, one host's share at 262144 tokens) for context.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 matrix-core peak (published)
+METRIC = "attention fwd / fwd+bwd TFLOPS and % of bf16 MFMA peak; tokens/s at seq 32K-256K"
+
+
+def causal_pairs(S):
+    return S * (S + 1) / 2
+
+
+def host_pairs(c, host, n_hosts):
+    """Visible (query, key) pairs of one host's query block under causal masking."""
+    return host * c * c + c * (c + 1) / 2
+
+
+def time_calls(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return e0.elapsed_time(e1) / steps, wall
+
+
+def cpu_baseline(B, S, H, D):
+    """fp64 oracle on one head of the workload, scaled to all heads."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import attention as OA
+    rng = np.random.default_rng(0)
+    q, k, v = (rng.standard_normal((B, S, 1, D)) for _ in range(3))
+    t0 = time.perf_counter()
+    OA.attention_fwd(q, k, v, True)
+    dt = time.perf_counter() - t0
+    flops_one_head = 4.0 * B * D * causal_pairs(S)
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {
+        "value": flops_one_head / dt / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": "oracle.attention.attention_fwd (fp64, NumPy BLAS) on 1 of %d heads of the "
+                  "workload (B=%d, S=%d, D=%d, causal): %.1f s; whole workload extrapolated "
+                  "linearly to %.0f s" % (H, B, S, D, dt, dt * H),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extra", action="store_true", help="skip the secondary configurations")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU's share of the virtual ring; --gpus %d is not "
+              "supported (the ring is emulated on a single device)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2310_01889_amd as ra
+
+    B, S, H, D, N = 1, 32768, 32, 128, 8
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2)
+    mk = lambda *shape: torch.randn(*shape, generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    q, k, v = mk(B, S, H, D), mk(B, S, H, D), mk(B, S, H, D)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, S), dtype=torch.float32, device="cuda")
+    step = lambda: ra.ring_attn_fwd(q, k, v, o, lse, N, True)
+
+    flops = 4.0 * B * H * D * causal_pairs(S)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ra.timing_read(ra.KERNEL_ATTN_FWD)
+    ra.timing_enable(True)
+    ms, wall = time_calls(step, args.steps, 0)
+    ra.timing_enable(False)
+    kms, launches = ra.timing_read(ra.KERNEL_ATTN_FWD)
+    k_avg_ms = kms / max(1, launches)
+    flops_per_launch = flops / N  # N launches per step
+    achieved = flops_per_launch / (k_avg_ms * 1e-3) / 1e12
+    value = flops / (ms * 1e-3) / 1e12
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic: N(0,1) bf16 q/k/v drawn on the GPU from a seeded generator",
+        "config": {"workload": "causal ring-attention forward, B=1 S=32768 H=32 D=128, "
+                               "8 virtual hosts x 4096-token blocks",
+                   "global_batch": B, "seq_len": S, "parallelism": "virtual ring of 8 hosts on 1 GPU"},
+        "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "tokens_per_s": round(B * S / (ms * 1e-3), 1),
+        "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (attention step)",
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "avg_launch_ms": round(k_avg_ms, 4), "launches": launches},
+    }
+
+    if not args.no_extra:
+        extra = {}
+        # forward + backward, B=1 S=16384 H=16 D=128, 8 hosts x 2048
+        B3, S3, H3, N3 = 1, 16384, 16, 8
+        q3, k3, v3, do3 = (mk(B3, S3, H3, D) for _ in range(4))
+        o3 = torch.empty_like(q3)
+        l3 = torch.empty((B3, H3, S3), dtype=torch.float32, device="cuda")
+        dq3, dk3, dv3 = torch.empty_like(q3), torch.empty_like(k3), torch.empty_like(v3)
+
+        def fb():
+            ra.ring_attn_fwd(q3, k3, v3, o3, l3, N3, True)
+            ra.ring_attn_bwd(q3, k3, v3, o3, l3, do3, dq3, dk3, dv3, N3, True)
+        ms3, _ = time_calls(fb, max(3, args.steps // 2), 2)
+        f3 = 4.0 * B3 * H3 * D * causal_pairs(S3) * 3.5
+        extra["fwd_bwd_S16384_H16"] = {"ms": round(ms3, 3), "tflops": round(f3 / ms3 / 1e9, 2),
+                                       "tokens_per_s": round(S3 / (ms3 * 1e-3), 1)}
+        del q3, k3, v3, do3, o3, dq3, dk3, dv3
+        # one host's share: host 7 of 8, 32768-token query block against 262144 keys
+        c5, N5, H5 = 32768, 8, 32
+        qb = mk(1, c5, H5, D)
+        k5, v5 = mk(1, N5 * c5, H5, D), mk(1, N5 * c5, H5, D)
+        ob = torch.empty_like(qb)
+        lb = torch.empty((1, H5, c5), dtype=torch.float32, device="cuda")
+        ms5, _ = time_calls(lambda: ra.ring_attn_fwd_host(qb, k5, v5, ob, lb, N5, 7, True), 3, 1)
+        f5 = 4.0 * H5 * D * host_pairs(c5, 7, N5)
+        extra["host7_of_8_c32768_H32"] = {"ms": round(ms5, 3), "tflops": round(f5 / ms5 / 1e9, 2),
+                                          "query_tokens_per_s": round(c5 / (ms5 * 1e-3), 1)}
+        out["extra"] = extra
+
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(B, S, H, D)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -165,6 +165,17 @@ int blockwise_linear_bwd(const void* x, const void* w, const void* dy, void* dx,
  * until the next library call on that thread. */
 const char* ring_attn_last_error(void);
 
+/*
+ * Kernel timing for benchmarks and profiling (not part of the method).
+ * ring_attn_timing_enable(1) makes every later launch of the library's hot kernels be
+ * bracketed by timing events on the stream it runs on; ring_attn_timing_read(kind, ...)
+ * waits for the recorded launches of that kind, returns their summed duration in
+ * milliseconds and their number, and forgets them.  Kinds:
+ */
+enum { RA_KERNEL_ATTN_FWD = 0, RA_KERNEL_ATTN_BWD = 1, RA_KERNEL_GEMM = 2 };
+void ring_attn_timing_enable(int on);
+int ring_attn_timing_read(int kind, double* total_ms, int* launches);
+
 #ifdef __cplusplus
 }
 #endif

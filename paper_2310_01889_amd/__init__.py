@@ -72,13 +72,37 @@ def load():
             fn.restype = ctypes.c_int
         lib.ring_attn_last_error.argtypes = []
         lib.ring_attn_last_error.restype = ctypes.c_char_p
+        lib.ring_attn_timing_enable.argtypes = [ctypes.c_int]
+        lib.ring_attn_timing_enable.restype = None
+        lib.ring_attn_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_int)]
+        lib.ring_attn_timing_read.restype = ctypes.c_int
         _LIB = lib
     return _LIB
 
 
 def exported_symbols():
     """Names of the C entry points the binding expects the library to export."""
-    return sorted(list(_SIGS) + ["ring_attn_last_error"])
+    return sorted(list(_SIGS) + ["ring_attn_last_error", "ring_attn_timing_enable",
+                                 "ring_attn_timing_read"])
+
+
+KERNEL_ATTN_FWD, KERNEL_ATTN_BWD, KERNEL_GEMM = 0, 1, 2
+
+
+def timing_enable(on=True):
+    """Bracket every later hot-kernel launch with timing events (ring_attn_timing_enable)."""
+    load().ring_attn_timing_enable(1 if on else 0)
+
+
+def timing_read(kind):
+    """(total milliseconds, launches) of the timed launches of ``kind`` since the last read."""
+    ms, n = ctypes.c_double(0.0), ctypes.c_int(0)
+    lib = load()
+    rc = lib.ring_attn_timing_read(int(kind), ctypes.byref(ms), ctypes.byref(n))
+    if rc != 0:
+        raise RingAttnError("ring_attn_timing_read", rc, lib.ring_attn_last_error().decode())
+    return ms.value, n.value
 
 
 def _call(name, *args):

@@ -33,6 +33,7 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const 
   if (row < nrows) {
     const bf16x8 a = *(const bf16x8*)(o + row * D + c);
     const bf16x8 g = *(const bf16x8*)(dO + row * D + c);
+    #pragma unroll
     for (int e = 0; e < 8; ++e) s = fmaf((float)a[e], (float)g[e], s);
   }
   for (int off = TPR / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
@@ -55,6 +56,7 @@ __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const 
   if (row < nrows) {
     const f32x4 a = *(const f32x4*)(o + row * D + c);
     const f32x4 g = *(const f32x4*)(dO + row * D + c);
+    #pragma unroll
     for (int e = 0; e < 4; ++e) s = fmaf(a[e], g[e], s);
   }
   for (int off = TPR / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
@@ -105,12 +107,15 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   const bf16* krow = (const bf16*)hs.k + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
   const bf16* vrow = (const bf16*)hs.v + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
   bf16x8 kreg[NKK], vreg[NKK];
+  #pragma unroll
   for (int kk = 0; kk < NKK; ++kk) {
     kreg[kk] = *(const bf16x8*)(krow + 16 * kk + 8 * hi);
     vreg[kk] = *(const bf16x8*)(vrow + 16 * kk + 8 * hi);
   }
   f32x16 dkacc[NDT], dvacc[NDT];
+  #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
+    #pragma unroll
     for (int i = 0; i < 16; ++i) dkacc[dt][i] = dvacc[dt][i] = 0.f;
 
   // query tiles with at least one query that sees a key of this workgroup
@@ -130,6 +135,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   u32x4 qpre[NPASS], opre[NPASS];
   float lpre = 0.f, dpre = 0.f;
   auto gload = [&](int qt) {
+    #pragma unroll
     for (int ps = 0; ps < NPASS; ++ps) {
       const long long off = (long long)(hs.q_row0 + qt * kQB + st_r + ps * RPP) * rs + st_c;
       qpre[ps] = *(const u32x4*)(qbase + off);
@@ -141,6 +147,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     }
   };
   auto lstore = [&](int buf) {
+    #pragma unroll
     for (int ps = 0; ps < NPASS; ++ps) {
       const int r = st_r + ps * RPP;
       *(u32x4*)(&sQ[buf][r * QS + st_c]) = qpre[ps];
@@ -166,18 +173,24 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
 
     // S = Q K^T : two 32-query tiles
     f32x16 sacc[2];
+    #pragma unroll
     for (int qm = 0; qm < 2; ++qm) {
+      #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[qm][i] = 0.f;
       const bf16* qr = &sQ[buf][(32 * qm + prow) * QS + 8 * hi];
+      #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) sacc[qm] = mfma32(*(const bf16x8*)(qr + 16 * kk), kreg[kk], sacc[qm]);
     }
     // P (queries 32qm + 16(i/8) + 8hi + i%8 of the tile)
     const bool need_mask = p.causal && (wg_first_k + kKB - 1 > qpos0);
+    #pragma unroll
     for (int qm = 0; qm < 2; ++qm)
+      #pragma unroll
       for (int hb = 0; hb < 2; ++hb) {
         const int q0 = 32 * qm + 16 * hb + 8 * hi;
         const f32x4 la = *(const f32x4*)&sL[buf][q0];
         const f32x4 lb = *(const f32x4*)&sL[buf][q0 + 4];
+        #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float lv = e < 4 ? la[e] : lb[e - 4];
           float pv = fast_exp2(fmaf(sacc[qm][8 * hb + e], sl2, -lv));
@@ -187,8 +200,10 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       }
     // dV^T += dO^T P
     bf16x8 pb[4];
+    #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       u32x4 w;
+      #pragma unroll
       for (int j = 0; j < 4; ++j)
         w[j] = pack_bf16x2(sacc[kb >> 1][8 * (kb & 1) + 2 * j], sacc[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
       pb[kb] = __builtin_bit_cast(bf16x8, w);
@@ -196,8 +211,10 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     const int g = lane >> 4, li = lane & 15;
     const int tcol = 16 * (g & 1) + 4 * (li & 3);
     const int trow = 8 * hi + (li >> 2);
+    #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       const bf16* op = &sO[buf][(16 * kb + trow) * QS + tcol];
+      #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         const bf16x4 lo = lds_read_tr16(op + 32 * dt);
         const bf16x4 up = lds_read_tr16(op + 4 * QS + 32 * dt);
@@ -206,15 +223,20 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       }
     }
     // dP = dO V^T, then dS = P * (dP - Delta)
+    #pragma unroll
     for (int qm = 0; qm < 2; ++qm) {
       f32x16 dp;
+      #pragma unroll
       for (int i = 0; i < 16; ++i) dp[i] = 0.f;
       const bf16* orr = &sO[buf][(32 * qm + prow) * QS + 8 * hi];
+      #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) dp = mfma32(*(const bf16x8*)(orr + 16 * kk), vreg[kk], dp);
+      #pragma unroll
       for (int hb = 0; hb < 2; ++hb) {
         const int q0 = 32 * qm + 16 * hb + 8 * hi;
         const f32x4 da = *(const f32x4*)&sD[buf][q0];
         const f32x4 db = *(const f32x4*)&sD[buf][q0 + 4];
+        #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float dv = e < 4 ? da[e] : db[e - 4];
           sacc[qm][8 * hb + e] = sacc[qm][8 * hb + e] * (dp[8 * hb + e] - dv);
@@ -222,12 +244,15 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       }
     }
     // dK^T += Q^T dS
+    #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       u32x4 w;
+      #pragma unroll
       for (int j = 0; j < 4; ++j)
         w[j] = pack_bf16x2(sacc[kb >> 1][8 * (kb & 1) + 2 * j], sacc[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
       const bf16x8 dsb = __builtin_bit_cast(bf16x8, w);
       const bf16* qp = &sQ[buf][(16 * kb + trow) * QS + tcol];
+      #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         const bf16x4 lo = lds_read_tr16(qp + 32 * dt);
         const bf16x4 up = lds_read_tr16(qp + 4 * QS + 32 * dt);
@@ -241,12 +266,15 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
 
   // add into the float32 gradient of the block (its home rows)
   const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key_in_blk) * rs + h * D;
+  #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
+    #pragma unroll
     for (int gg = 0; gg < 4; ++gg) {
       const int d = 32 * dt + 8 * gg + 4 * hi;
       f32x4* dkp = (f32x4*)(p.dk + grow + d);
       f32x4* dvp = (f32x4*)(p.dv + grow + d);
       f32x4 k4 = *dkp, v4 = *dvp;
+      #pragma unroll
       for (int e = 0; e < 4; ++e) {
         k4[e] += dkacc[dt][4 * gg + e] * p.scale;
         v4[e] += dvacc[dt][4 * gg + e];
@@ -297,13 +325,16 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
   bf16x8 qreg[NKK], oreg[NKK];
   {
     const long long off = (long long)b * p.q_bstride + (long long)qr * rs + h * D + 8 * hi;
+    #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
       qreg[kk] = *(const bf16x8*)((const bf16*)p.q + off + 16 * kk);
       oreg[kk] = *(const bf16x8*)((const bf16*)p.dO + off + 16 * kk);
     }
   }
   f32x16 dqacc[NDT];
+  #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
+    #pragma unroll
     for (int i = 0; i < 16; ++i) dqacc[dt][i] = 0.f;
 
   int nt = p.c / kKK;
@@ -316,6 +347,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
   const int st_r = tid / CPR, st_c = (tid % CPR) * 8;
   u32x4 kpre[NPASS], vpre[NPASS];
   auto gload = [&](int it) {
+    #pragma unroll
     for (int ps = 0; ps < NPASS; ++ps) {
       const long long off = (long long)(it * kKK + st_r + ps * RPP) * rs + st_c;
       kpre[ps] = *(const u32x4*)(kbase + off);
@@ -323,6 +355,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
     }
   };
   auto lstore = [&](int buf) {
+    #pragma unroll
     for (int ps = 0; ps < NPASS; ++ps) {
       const int r = st_r + ps * RPP;
       *(u32x4*)(&sK[buf][r * KS + st_c]) = kpre[ps];
@@ -340,10 +373,13 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
     const int buf = it & 1;
     if (it + 1 < nt) gload(it + 1);
     f32x16 sacc[2], dpacc[2];
+    #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
+      #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[mt][i] = dpacc[mt][i] = 0.f;
       const bf16* kr = &sK[buf][(32 * mt + krow_perm) * KS + 8 * hi];
       const bf16* vr = &sV[buf][(32 * mt + krow_perm) * KS + 8 * hi];
+      #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
         sacc[mt] = mfma32(*(const bf16x8*)(kr + 16 * kk), qreg[kk], sacc[mt]);
         dpacc[mt] = mfma32(*(const bf16x8*)(vr + 16 * kk), oreg[kk], dpacc[mt]);
@@ -352,10 +388,13 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
     const int kpos0 = hs.k_pos0 + it * kKK;
     const bool need_mask = p.causal && (kpos0 + kKK - 1 > tile_first_q);
     bf16x8 dsb[4];
+    #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       u32x4 w;
+      #pragma unroll
       for (int j = 0; j < 4; ++j) {
         float ds2[2];
+        #pragma unroll
         for (int e = 0; e < 2; ++e) {
           const int i = 8 * (kb & 1) + 2 * j + e;
           const int mt = kb >> 1;
@@ -374,8 +413,10 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
     const int g = lane >> 4, li = lane & 15;
     const int tcol = 16 * (g & 1) + 4 * (li & 3);
     const int trow = 8 * hi + (li >> 2);
+    #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       const bf16* kp = &sK[buf][(16 * kb + trow) * KS + tcol];
+      #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         const bf16x4 lo = lds_read_tr16(kp + 32 * dt);
         const bf16x4 up = lds_read_tr16(kp + 4 * KS + 32 * dt);
@@ -388,11 +429,14 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
   }
   // dq (float32, [B, Sq, H, D]) += scale * dQ
   float* dqrow = p.dq + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+  #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
+    #pragma unroll
     for (int gg = 0; gg < 4; ++gg) {
       const int d = 32 * dt + 8 * gg + 4 * hi;
       f32x4* dp = (f32x4*)(dqrow + d);
       f32x4 t = *dp;
+      #pragma unroll
       for (int e = 0; e < 4; ++e) t[e] += dqacc[dt][4 * gg + e] * p.scale;
       *dp = t;
     }
@@ -422,6 +466,7 @@ __global__ __launch_bounds__(64) void bwd_dkdv_f32_kernel(const BwdStep p) {
   const float* kr = (const float*)hs.k + (long long)b * hs.kv_bstride + (long long)key * rs + h * D;
   const float* vr = (const float*)hs.v + (long long)b * hs.kv_bstride + (long long)key * rs + h * D;
   float k[D], v[D], dk[D], dv[D];
+  #pragma unroll
   for (int d = 0; d < D; ++d) {
     k[d] = kr[d];
     v[d] = vr[d];
@@ -449,12 +494,14 @@ __global__ __launch_bounds__(64) void bwd_dkdv_f32_kernel(const BwdStep p) {
       const int qpos = hs.q_pos0 + q0 + j;
       if (p.causal && kpos > qpos) continue;
       float s = 0.f, dp = 0.f;
+      #pragma unroll
       for (int d = 0; d < D; ++d) {
         s = fmaf(sQ[j * D + d], k[d], s);
         dp = fmaf(sO[j * D + d], v[d], dp);
       }
       const float pr = expf(s * p.scale - sL[j]);
       const float ds = pr * (dp - sD[j]);
+      #pragma unroll
       for (int d = 0; d < D; ++d) {
         dv[d] = fmaf(pr, sO[j * D + d], dv[d]);
         dk[d] = fmaf(ds, sQ[j * D + d], dk[d]);
@@ -462,6 +509,7 @@ __global__ __launch_bounds__(64) void bwd_dkdv_f32_kernel(const BwdStep p) {
     }
   }
   const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key) * rs + h * D;
+  #pragma unroll
   for (int d = 0; d < D; ++d) {
     p.dk[grow + d] += dk[d] * p.scale;
     p.dv[grow + d] += dv[d];
@@ -487,6 +535,7 @@ __global__ __launch_bounds__(64) void bwd_dq_f32_kernel(const BwdStep p) {
   const float lse = p.lse[lrow], dlt = p.delta[lrow];
   const long long qoff = (long long)b * p.q_bstride + (long long)qr * rs + h * D;
   float q[D], o[D], dq[D];
+  #pragma unroll
   for (int d = 0; d < D; ++d) {
     q[d] = ((const float*)p.q)[qoff + d];
     o[d] = ((const float*)p.dO)[qoff + d];
@@ -507,15 +556,18 @@ __global__ __launch_bounds__(64) void bwd_dq_f32_kernel(const BwdStep p) {
     for (int j = 0; j < kFT; ++j) {
       if (p.causal && hs.k_pos0 + k0 + j > qpos) continue;
       float s = 0.f, dp = 0.f;
+      #pragma unroll
       for (int d = 0; d < D; ++d) {
         s = fmaf(q[d], sK[j * D + d], s);
         dp = fmaf(o[d], sV[j * D + d], dp);
       }
       const float ds = expf(s * p.scale - lse) * (dp - dlt);
+      #pragma unroll
       for (int d = 0; d < D; ++d) dq[d] = fmaf(ds, sK[j * D + d], dq[d]);
     }
   }
   float* dqrow = p.dq + qoff;
+  #pragma unroll
   for (int d = 0; d < D; ++d) dqrow[d] += dq[d] * p.scale;
 }
 

@@ -82,14 +82,19 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   const long long st_row = (long long)bh * p.Sq + qr;
   float* acc_tile = p.acc + ((long long)bh * (p.Sq / kBM) + q_tile_row / kBM) * (kBM * D);
   if (hs.flags & kFirst) {
+    #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
+      #pragma unroll
       for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
     m_run = -INFINITY;
     l_run = 0.f;
   } else {
+    #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
+      #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 t = ((const f32x4*)acc_tile)[((wave * NDT + dt) * 4 + g) * 64 + lane];
+        #pragma unroll
         for (int e = 0; e < 4; ++e) oacc[dt][4 * g + e] = t[e];
       }
     m_run = p.m[st_row];
@@ -100,6 +105,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   bf16x8 qreg[NKK];
   {
     const bf16* qrow = qbase + (long long)qr * rs;
+    #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) qreg[kk] = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
   }
 
@@ -108,6 +114,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   u32x4 kpre[NPASS], vpre[NPASS];
   auto gload = [&](int it) {
     const int r0 = it * kBN + st_row_in_pass;
+    #pragma unroll
     for (int ps = 0; ps < NPASS; ++ps) {
       const long long off = (long long)(r0 + ps * RPP) * rs + st_col;
       kpre[ps] = *(const u32x4*)(kbase + off);
@@ -115,6 +122,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     }
   };
   auto lstore = [&](int buf) {
+    #pragma unroll
     for (int ps = 0; ps < NPASS; ++ps) {
       const int r = st_row_in_pass + ps * RPP;
       *(u32x4*)(&sK[buf][r * KS + st_col]) = kpre[ps];
@@ -137,9 +145,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
 
     // S^T = K Q^T for 64 keys x 32 queries: two 32-key tiles
     f32x16 sacc[2];
+    #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
+      #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[mt][i] = 0.f;
       const bf16* krow = &sK[buf][(32 * mt + krow_perm) * KS + 8 * hi];
+      #pragma unroll
       for (int kk = 0; kk < NKK; ++kk)
         sacc[mt] = mfma32(*(const bf16x8*)(krow + 16 * kk), qreg[kk], sacc[mt]);
     }
@@ -147,7 +158,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     // causal mask: only tiles whose last key lies after the workgroup's first query
     const int kpos0 = hs.k_pos0 + it * kBN;
     if (p.causal && kpos0 + kBN - 1 > tile_first_q) {
+      #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
+        #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
           if (kpos > qpos) sacc[mt][i] = -INFINITY;
@@ -157,7 +170,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     // online softmax (log2 domain): each lane owns one query, the partner lane l^32
     // holds the other half of its keys
     float mx = -INFINITY;
+    #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
+      #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[mt][i]);
     mx = pair_max(mx);
     const float m_new = fmaxf(m_run, mx * sl2);
@@ -166,8 +181,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     m_run = m_new;
     float rsum = 0.f;
     bf16x8 pb[4];
+    #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       uint32_t w[4];
+      #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float p0 = fast_exp2(fmaf(sacc[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
         const float p1 = fast_exp2(fmaf(sacc[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
@@ -178,7 +195,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       pb[kb] = __builtin_bit_cast(bf16x8, wv);
     }
     l_run = l_run * alpha + rsum;
+    #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
+      #pragma unroll
       for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
 
     // O^T += V^T P^T: A operand = V^T (m = dim, k = key) via LDS transpose reads
@@ -186,8 +205,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       const int g = lane >> 4, li = lane & 15;
       const int dcol = 16 * (g & 1) + 4 * (li & 3);
       const int krow = 8 * hi + (li >> 2);
+      #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         const bf16* vp = &sV[buf][(16 * kb + krow) * VS + dcol];
+        #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
           const bf16x4 lo = lds_read_tr16(vp + 32 * dt);
           const bf16x4 up = lds_read_tr16(vp + 4 * VS + 32 * dt);
@@ -206,7 +227,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   if (hs.flags & kLast) {
     const float inv = 1.f / l_tot;
     bf16* orow = (bf16*)p.o + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+    #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
+      #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int d = 32 * dt + 8 * g + 4 * hi;
         u32x2 w = {pack_bf16x2(oacc[dt][4 * g] * inv, oacc[dt][4 * g + 1] * inv),
@@ -215,7 +238,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       }
     if (!hi) p.lse[st_row] = m_run * kLn2 + logf(l_tot);
   } else {
+    #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
+      #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 t = {oacc[dt][4 * g], oacc[dt][4 * g + 1], oacc[dt][4 * g + 2], oacc[dt][4 * g + 3]};
         ((f32x4*)acc_tile)[((wave * NDT + dt) * 4 + g) * 64 + lane] = t;
@@ -258,13 +283,16 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(const FwdStep p) {
   float* accrow = p.acc + st_row * D;
 
   float q[D], acc[D];
+  #pragma unroll
   for (int d = 0; d < D; ++d) q[d] = qrow[d];
   float m_run, l_run;
   if (hs.flags & kFirst) {
+    #pragma unroll
     for (int d = 0; d < D; ++d) acc[d] = 0.f;
     m_run = -INFINITY;
     l_run = 0.f;
   } else {
+    #pragma unroll
     for (int d = 0; d < D; ++d) acc[d] = accrow[d];
     m_run = p.m[st_row];
     l_run = p.l[st_row];
@@ -286,8 +314,10 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(const FwdStep p) {
     __syncthreads();
     float s[kF32BN];
     float mx = -INFINITY;
+    #pragma unroll
     for (int j = 0; j < kF32BN; ++j) {
       float dot = 0.f;
+      #pragma unroll
       for (int d = 0; d < D; ++d) dot = fmaf(q[d], sK[j * D + d], dot);
       const int kpos = hs.k_pos0 + it * kF32BN + j;
       s[j] = (p.causal && kpos > qpos) ? -INFINITY : dot * p.scale;
@@ -298,18 +328,23 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(const FwdStep p) {
     const float alpha = expf(m_run - m_use);
     m_run = m_new;
     l_run *= alpha;
+    #pragma unroll
     for (int d = 0; d < D; ++d) acc[d] *= alpha;
+    #pragma unroll
     for (int j = 0; j < kF32BN; ++j) {
       const float pj = expf(s[j] - m_use);
       l_run += pj;
+      #pragma unroll
       for (int d = 0; d < D; ++d) acc[d] = fmaf(pj, sV[j * D + d], acc[d]);
     }
   }
   if (hs.flags & kLast) {
     float* orow = (float*)p.o + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+    #pragma unroll
     for (int d = 0; d < D; ++d) orow[d] = acc[d] / l_run;
     p.lse[st_row] = m_run + logf(l_run);
   } else {
+    #pragma unroll
     for (int d = 0; d < D; ++d) accrow[d] = acc[d];
     p.m[st_row] = m_run;
     p.l[st_row] = l_run;

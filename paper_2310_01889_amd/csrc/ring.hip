@@ -21,6 +21,7 @@
 
 #include "ra_common.h"
 #include "ra_kernels.h"
+#include "ra_runtime.h"
 #include "ringattn.h"
 
 namespace ra {
@@ -37,13 +38,6 @@ int set_err(int code, const char* fmt, ...) {
   return code;
 }
 
-#define RA_HIP(expr)                                                                   \
-  do {                                                                                 \
-    hipError_t e_ = (expr);                                                            \
-    if (e_ != hipSuccess)                                                              \
-      return set_err(e_ == hipErrorOutOfMemory ? RA_ENOMEM : RA_EHIP, "%s failed: %s", \
-                     #expr, hipGetErrorString(e_));                                    \
-  } while (0)
 
 // ---------------------------------------------------------------------------------
 // Per-device side stream (created once, default priority) and memory-pool setting.
@@ -71,32 +65,32 @@ int side_stream(hipStream_t* out) {
   return RA_OK;
 }
 
+// ---------------------------------------------------------------------------------
+// Optional per-kernel timing (benchmarks): when enabled, every step-kernel launch is
+// bracketed by timing events on the stream it is launched on.
+// ---------------------------------------------------------------------------------
+namespace {
+std::mutex g_tmu;
+bool g_timing = false;
+struct TimedLaunch { int kind; hipEvent_t a, b; };
+std::vector<TimedLaunch> g_timed;
+}  // namespace
+
+bool timing_on() {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  return g_timing;
+}
+
+void timing_push(int kind, hipEvent_t a, hipEvent_t b) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timed.push_back({kind, a, b});
+}
+
 static bool env_flag(const char* name) {
   const char* v = getenv(name);
   return v && v[0] && v[0] != '0';
 }
 
-// Stream-ordered workspace and events owned by one call; released on every exit path.
-struct CallResources {
-  hipStream_t stream;
-  void* ws = nullptr;
-  std::vector<hipEvent_t> events;
-  explicit CallResources(hipStream_t s) : stream(s) {}
-  ~CallResources() {
-    if (ws) (void)hipFreeAsync(ws, stream);
-    for (hipEvent_t e : events) (void)hipEventDestroy(e);
-  }
-  int alloc(size_t bytes) {
-    if (bytes == 0) return RA_OK;
-    RA_HIP(hipMallocAsync(&ws, bytes, stream));
-    return RA_OK;
-  }
-  int event(hipEvent_t* e) {
-    RA_HIP(hipEventCreateWithFlags(e, hipEventDisableTiming));
-    events.push_back(*e);
-    return RA_OK;
-  }
-};
 
 // ---------------------------------------------------------------------------------
 // Ring plan shared by forward and backward.
@@ -286,7 +280,9 @@ static int run_fwd(const RingProblem& P, void* o, float* lse, hipStream_t stream
                                           const std::vector<int>&) -> int {
     st.n_slots = (int)hs.size();
     for (size_t s = 0; s < hs.size(); ++s) st.host[s] = hs[s];
-    RA_HIP(P.elt == 2 ? launch_fwd_bf16(st, P.D, stream) : launch_fwd_f32(st, P.D, stream));
+    RA_HIP(timed_launch(RA_KERNEL_ATTN_FWD, stream, [&] {
+      return P.elt == 2 ? launch_fwd_bf16(st, P.D, stream) : launch_fwd_f32(st, P.D, stream);
+    }));
     return RA_OK;
   });
 }
@@ -341,7 +337,9 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
       st.host[s] = hs[s];
       st.dkv_row0[s] = blks[s] * P.c();
     }
-    RA_HIP(f32 ? launch_bwd_f32(st, P.D, stream) : launch_bwd_bf16(st, P.D, stream));
+    RA_HIP(timed_launch(RA_KERNEL_ATTN_BWD, stream, [&] {
+      return f32 ? launch_bwd_f32(st, P.D, stream) : launch_bwd_bf16(st, P.D, stream);
+    }));
     return RA_OK;
   });
   if (rc) return rc;
@@ -384,6 +382,38 @@ using namespace ra;
 extern "C" {
 
 const char* ring_attn_last_error(void) { return g_err.c_str(); }
+
+void ring_attn_timing_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = on != 0;
+}
+
+int ring_attn_timing_read(int kind, double* total_ms, int* launches) {
+  g_err.clear();
+  if (!total_ms || !launches) return set_err(RA_EINVAL, "null pointer argument");
+  std::vector<TimedLaunch> mine, rest;
+  {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    for (const TimedLaunch& t : g_timed) (t.kind == kind ? mine : rest).push_back(t);
+    g_timed.swap(rest);
+  }
+  double sum = 0;
+  int rc = RA_OK;
+  for (const TimedLaunch& t : mine) {
+    float ms = 0.f;
+    if (rc == RA_OK) {
+      hipError_t e = hipEventSynchronize(t.b);
+      if (e == hipSuccess) e = hipEventElapsedTime(&ms, t.a, t.b);
+      if (e != hipSuccess) rc = set_err(RA_EHIP, "timing event: %s", hipGetErrorString(e));
+    }
+    sum += ms;
+    (void)hipEventDestroy(t.a);
+    (void)hipEventDestroy(t.b);
+  }
+  *total_ms = sum;
+  *launches = (int)mine.size();
+  return rc;
+}
 
 int ring_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S, int D,
                   int n_hosts, int causal, hipStream_t stream) {

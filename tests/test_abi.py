@@ -1,0 +1,88 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point its
+header declares, and rejects invalid arguments with the documented status codes before
+touching the device (pointer arguments here are never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2310_01889_amd as ra
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ringattn.h")
+
+RA_OK, RA_EINVAL, RA_EUNSUPPORTED = 0, 1, 2
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+NULL = ctypes.c_void_p(0)
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?(?:int|void|char)\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ra.library_path()):
+        pytest.skip("library not built")
+    return ra.load()
+
+
+def test_header_declares_what_the_binding_expects():
+    assert header_functions() == ra.exported_symbols()
+
+
+def test_library_exports_every_header_symbol(lib):
+    for name in header_functions():
+        assert hasattr(lib, name), name
+
+
+def _fwd(lib, *, q=FAKE, B=1, H=1, S=1024, D=128, N=4, causal=1):
+    return lib.ring_attn_fwd(q, FAKE, FAKE, FAKE, FAKE, B, H, S, D, N, causal, NULL)
+
+
+def test_attention_argument_validation(lib):
+    assert _fwd(lib, q=NULL) == RA_EINVAL
+    assert b"null" in lib.ring_attn_last_error()
+    assert _fwd(lib, B=0) == RA_EINVAL
+    assert _fwd(lib, N=0) == RA_EINVAL
+    assert _fwd(lib, causal=2) == RA_EINVAL
+    assert _fwd(lib, D=96) == RA_EUNSUPPORTED
+    assert _fwd(lib, N=3) == RA_EUNSUPPORTED          # S % n_hosts
+    assert _fwd(lib, S=1024, N=16) == RA_EUNSUPPORTED  # block 64 not a multiple of 128
+    assert _fwd(lib, N=65, S=65 * 128) == RA_EUNSUPPORTED
+    assert _fwd(lib, B=1 << 10, H=64, S=1 << 16) == RA_EUNSUPPORTED  # > 2^31 elements
+    assert b"2^31" in lib.ring_attn_last_error()
+    # float32 variant accepts 64-token blocks but not 32
+    assert lib.ring_attn_fwd_f32(FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 1024, 64, 32, 1, NULL) == RA_EUNSUPPORTED
+    assert lib.ring_attn_fwd_host(FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 1024, 128, 4, 4, 1, NULL) == RA_EINVAL
+    bad = (ctypes.c_int * 4)(0, 0, 1, 0)  # row 0 repeats block 0
+    assert lib.ring_attn_fwd_ordered(FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 512, 128, 2, 1,
+                                     ctypes.cast(bad, ctypes.c_void_p), NULL) == RA_EINVAL
+    assert b"permutation" in lib.ring_attn_last_error()
+    assert lib.ring_attn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NULL,
+                             1, 1, 1024, 128, 4, 1, NULL) == RA_EINVAL
+
+
+def test_ffn_argument_validation(lib):
+    f = lib.blockwise_ffn
+    assert f(FAKE, FAKE, NULL, FAKE, NULL, FAKE, 512, 256, 512, 256, 5, NULL) == RA_EINVAL
+    assert f(FAKE, FAKE, NULL, FAKE, NULL, FAKE, 500, 256, 512, 250, 0, NULL) == RA_EUNSUPPORTED
+    assert f(FAKE, FAKE, NULL, FAKE, NULL, FAKE, 512, 256, 500, 256, 0, NULL) == RA_EUNSUPPORTED
+    assert f(NULL, FAKE, NULL, FAKE, NULL, FAKE, 512, 256, 512, 256, 0, NULL) == RA_EINVAL
+    assert lib.blockwise_linear(FAKE, FAKE, NULL, FAKE, 512, 256, 300, 256, NULL) == RA_EUNSUPPORTED
+    assert lib.blockwise_linear_bwd(FAKE, FAKE, FAKE, NULL, NULL, 512, 256, 256, 256, NULL) == RA_EINVAL
+    assert lib.blockwise_ffn_bwd(FAKE, FAKE, NULL, FAKE, FAKE, FAKE, FAKE, NULL, FAKE, NULL,
+                                 512, 256, 512, 256, 3, NULL) == RA_EINVAL
+
+
+def test_product_path_does_not_use_the_oracle():
+    """The package never imports the CPU oracle (it would be a silent CPU fallback)."""
+    pkg = os.path.join(ROOT, "paper_2310_01889_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(from|import)\s+oracle\b", text, flags=re.M), f
