@@ -10,6 +10,8 @@
 // with s = q k^T / sqrt(D), masked (causal, by global position) keys giving p = 0.
 // On a host's first active step the state starts from (m=-inf, l=0, acc=0) in
 // registers; on its last it is finalised into o = acc / l and lse = m + ln l.
+#include <type_traits>
+
 #include "ra_common.h"
 #include "ra_kernels.h"
 
@@ -29,22 +31,41 @@ namespace ra {
 namespace {
 
 constexpr int kBM = 128, kBN = 64, kThreads = 256;
+constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units)
 
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
+// LDS tiles are unpadded [64 rows][D] with the 16-byte chunks of each row permuted by
+// an XOR swizzle, so that every read pattern below is free of bank conflicts:
+//   * row reads (A operand of S^T): 16 lanes read 16 consecutive rows at one chunk;
+//   * transpose reads (V^T): 16 lanes read 4 consecutive rows x 32 contiguous bytes.
+// For D = 128 (16 chunks per row): chunk c of row r lives at c ^ (4 (r & 3) + ((r >> 2) & 3));
+// for D = 64 (8 chunks, two rows per 256-byte bank sweep) at c ^ s, s = (r >> 1) & 7 with
+// bit 2 flipped on odd s.  Tiles are filled with direct-to-LDS loads (no registers):
+// lane i of a 1 KB load lands at byte 16 i of its destination, so each lane fetches the
+// logical chunk that the swizzle puts there.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) {
+    return 4 * (r & 3) + ((r >> 2) & 3);
+  } else {
+    const int s = (r >> 1) & 7;
+    return s ^ ((s & 1) << 2);
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) {
-  constexpr int KS = D + 8;    // LDS row stride of the K tile (elements)
-  constexpr int VS = D + 32;   // LDS row stride of the V tile (elements)
   constexpr int NKK = D / 16;  // 16-wide reduction steps of q.k
   constexpr int NDT = D / 32;  // 32-row output tiles of O^T
-  constexpr int CPR = D / 8;                  // 16-byte chunks per row
-  constexpr int RPP = kThreads / CPR;         // rows per staging pass
-  constexpr int NPASS = kBN / RPP;            // staging passes per tile
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][kBN * KS];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][kBN * VS];
+  constexpr int CPR = D / 8;   // 16-byte chunks per row
+  constexpr int ROWS_PER_LOAD = 64 / CPR;               // rows filled by one 1 KB wave load
+  constexpr int LOADS = kBN / 4 / ROWS_PER_LOAD;        // loads per wave per tile (16 rows/wave)
+  constexpr int TILE = kBN * D;                          // elements per tile
+  __shared__ __attribute__((aligned(1024))) bf16 sK[2][TILE];
+  __shared__ __attribute__((aligned(1024))) bf16 sV[2][TILE];
 
   const int n_qt = p.c / kBM;
   const int BH = p.B * p.H;
@@ -69,11 +90,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   const bf16* kbase = (const bf16*)hs.k + (long long)b * hs.kv_bstride + h * D;
   const bf16* vbase = (const bf16*)hs.v + (long long)b * hs.kv_bstride + h * D;
 
-  // number of key tiles with at least one visible key for this workgroup
-  int nt = p.c / kBN;
+  // key tiles with at least one visible key; the first n_full need no mask
+  int nt = p.c / kBN, n_full = nt;
   if (p.causal) {
     const int vis = tile_first_q + kBM - hs.k_pos0;  // keys visible to the last row
     nt = min(nt, max(0, (vis + kBN - 1) / kBN));
+    n_full = min(nt, max(0, (tile_first_q - hs.k_pos0 + 1) / kBN));
   }
 
   // ---- running state -------------------------------------------------------------
@@ -82,19 +104,19 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   const long long st_row = (long long)bh * p.Sq + qr;
   float* acc_tile = p.acc + ((long long)bh * (p.Sq / kBM) + q_tile_row / kBM) * (kBM * D);
   if (hs.flags & kFirst) {
-    #pragma unroll
+#pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
-      #pragma unroll
+#pragma unroll
       for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
     m_run = -INFINITY;
     l_run = 0.f;
   } else {
-    #pragma unroll
+#pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
-      #pragma unroll
+#pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 t = ((const f32x4*)acc_tile)[((wave * NDT + dt) * 4 + g) * 64 + lane];
-        #pragma unroll
+#pragma unroll
         for (int e = 0; e < 4; ++e) oacc[dt][4 * g + e] = t[e];
       }
     m_run = p.m[st_row];
@@ -105,131 +127,166 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   bf16x8 qreg[NKK];
   {
     const bf16* qrow = qbase + (long long)qr * rs;
-    #pragma unroll
+#pragma unroll
     for (int kk = 0; kk < NKK; ++kk) qreg[kk] = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
   }
 
-  // ---- staging helpers ---------------------------------------------------------------
-  const int st_row_in_pass = tid / CPR, st_col = (tid % CPR) * 8;
-  u32x4 kpre[NPASS], vpre[NPASS];
-  auto gload = [&](int it) {
-    const int r0 = it * kBN + st_row_in_pass;
-    #pragma unroll
-    for (int ps = 0; ps < NPASS; ++ps) {
-      const long long off = (long long)(r0 + ps * RPP) * rs + st_col;
-      kpre[ps] = *(const u32x4*)(kbase + off);
-      vpre[ps] = *(const u32x4*)(vbase + off);
-    }
+  // ---- direct-to-LDS staging: each wave fills 16 rows of a tile ---------------------
+  // load j of a wave covers rows wave*16 + j*ROWS_PER_LOAD + lane / CPR; the lane's
+  // physical chunk is lane % CPR, its logical (global) chunk that ^ swz(row).
+  int goff[LOADS];
+#pragma unroll
+  for (int j = 0; j < LOADS; ++j) {
+    const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
+    goff[j] = r * rs + 8 * ((lane % CPR) ^ swz<D>(r));
+  }
+  auto dload = [&](const bf16* src_tile, bf16* dst_tile) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(src_tile + goff[j]),
+                                       (lds_void*)(dst_tile + (wave * 16 + j * ROWS_PER_LOAD) * D), 16, 0, 0);
   };
-  auto lstore = [&](int buf) {
-    #pragma unroll
-    for (int ps = 0; ps < NPASS; ++ps) {
-      const int r = st_row_in_pass + ps * RPP;
-      *(u32x4*)(&sK[buf][r * KS + st_col]) = kpre[ps];
-      *(u32x4*)(&sV[buf][r * VS + st_col]) = vpre[ps];
+  auto load_k = [&](int it, int buf) __attribute__((always_inline)) { dload(kbase + (long long)it * kBN * rs, sK[buf]); };
+  auto load_v = [&](int it, int buf) __attribute__((always_inline)) { dload(vbase + (long long)it * kBN * rs, sV[buf]); };
+
+  // ---- per-lane LDS read offsets (elements), fixed across tiles ----------------------
+  // row reads of K: row 32 mt + swap_bits23(l32), logical chunk 2 kk + hi
+  const int krow = swap_bits23(l32);
+  int koff[NKK];
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk) koff[kk] = krow * D + 8 * ((2 * kk + hi) ^ swz<D>(krow));
+  // transpose reads of V: rows 16 kb + 8 hi + 4 r + li / 4, dims 32 dt + 16 (g & 1) + 4 (li & 3)
+  const int g16 = lane >> 4, li = lane & 15;
+  int voff[2][NDT];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const int row = 8 * hi + 4 * r + (li >> 2);
+      const int d = 32 * dt + 16 * (g16 & 1) + 4 * (li & 3);
+      voff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
-  };
 
   const float sl2 = p.scale * kLog2e;
-  const int krow_perm = swap_bits23(l32);
-
-  if (nt > 0) {
-    gload(0);
-    lstore(0);
-  }
-  __syncthreads();
-
-  for (int it = 0; it < nt; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < nt) gload(it + 1);
-
-    // S^T = K Q^T for 64 keys x 32 queries: two 32-key tiles
-    f32x16 sacc[2];
-    #pragma unroll
+  // S^T = K Q^T for the 64 keys of K buffer `buf` x this wave's 32 queries
+  auto scores = [&](const bf16* kt, f32x16* sacc) __attribute__((always_inline)) {
+#pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      #pragma unroll
+#pragma unroll
       for (int i = 0; i < 16; ++i) sacc[mt][i] = 0.f;
-      const bf16* krow = &sK[buf][(32 * mt + krow_perm) * KS + 8 * hi];
-      #pragma unroll
+#pragma unroll
       for (int kk = 0; kk < NKK; ++kk)
-        sacc[mt] = mfma32(*(const bf16x8*)(krow + 16 * kk), qreg[kk], sacc[mt]);
+        sacc[mt] = mfma32(*(const bf16x8*)(kt + 32 * mt * D + koff[kk]), qreg[kk], sacc[mt]);
     }
+  };
 
-    // causal mask: only tiles whose last key lies after the workgroup's first query
-    const int kpos0 = hs.k_pos0 + it * kBN;
-    if (p.causal && kpos0 + kBN - 1 > tile_first_q) {
-      #pragma unroll
+  // ---- pipeline: K runs one tile ahead of V ------------------------------------------
+  // While tile it is processed, LDS holds K tiles it, it+1 and V tile it; loads of K tile
+  // it+2 (into the buffer of K tile it) and V tile it+1 (into the buffer of V tile it-1)
+  // are in flight.  The scores of tile it+1 are formed on the matrix cores while the
+  // softmax of tile it runs on the vector ALUs.
+  if (nt > 0) {
+    load_k(0, 0);
+    load_v(0, 0);
+    if (nt > 1) load_k(1, 1);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  f32x16 s_cur[2];
+  if (nt > 0) scores(sK[0], s_cur);
+
+  auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value;     // it & 1
+    constexpr bool MASK = decltype(Mc)::value;  // tile may hold keys after some query
+    if (it + 2 < nt) load_k(it + 2, B);
+    if (it + 1 < nt) load_v(it + 1, B ^ 1);
+    f32x16 s_next[2];
+    const bool has_next = it + 1 < nt;
+    if (has_next) scores(sK[B ^ 1], s_next);
+
+    if (MASK) {
+      const int kpos0 = hs.k_pos0 + it * kBN;
+#pragma unroll
       for (int mt = 0; mt < 2; ++mt)
-        #pragma unroll
+#pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
-          if (kpos > qpos) sacc[mt][i] = -INFINITY;
+          if (kpos > qpos) s_cur[mt][i] = -INFINITY;
         }
     }
-
-    // online softmax (log2 domain): each lane owns one query, the partner lane l^32
-    // holds the other half of its keys
+    // online softmax, log2 domain; each lane owns one query and the partner lane l^32
+    // holds the other half of its keys.  The running maximum is raised only when a row's
+    // new maximum exceeds it by more than kTau (probabilities then stay below 2^kTau), so
+    // the rescale of the accumulator -- a wave-uniform branch -- is rare.
     float mx = -INFINITY;
-    #pragma unroll
+#pragma unroll
     for (int mt = 0; mt < 2; ++mt)
-      #pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[mt][i]);
-    mx = pair_max(mx);
-    const float m_new = fmaxf(m_run, mx * sl2);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    m_run = m_new;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s_cur[mt][i]);
+    const float mx2 = pair_max(mx) * sl2;
+    if (__builtin_amdgcn_ballot_w64(mx2 > m_run + kTau)) {
+      const float m_new = fmaxf(m_run, mx2);
+      const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float rsum = 0.f;
-    bf16x8 pb[4];
-    #pragma unroll
+    const bf16* vt = sV[B];
+#pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      uint32_t w[4];
-      #pragma unroll
+      u32x4 w;
+#pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p0 = fast_exp2(fmaf(sacc[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
-        const float p1 = fast_exp2(fmaf(sacc[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
+        const float p0 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
+        const float p1 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
         rsum += p0 + p1;
         w[j] = pack_bf16x2(p0, p1);
       }
-      u32x4 wv = {w[0], w[1], w[2], w[3]};
-      pb[kb] = __builtin_bit_cast(bf16x8, wv);
-    }
-    l_run = l_run * alpha + rsum;
-    #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-      #pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
-
-    // O^T += V^T P^T: A operand = V^T (m = dim, k = key) via LDS transpose reads
-    {
-      const int g = lane >> 4, li = lane & 15;
-      const int dcol = 16 * (g & 1) + 4 * (li & 3);
-      const int krow = 8 * hi + (li >> 2);
-      #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const bf16* vp = &sV[buf][(16 * kb + krow) * VS + dcol];
-        #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          const bf16x4 lo = lds_read_tr16(vp + 32 * dt);
-          const bf16x4 up = lds_read_tr16(vp + 4 * VS + 32 * dt);
-          const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-          oacc[dt] = mfma32(a, pb[kb], oacc[dt]);
-        }
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, w);
+      // O^T += V^T P^T for these 16 keys: A operand = V^T via LDS transpose reads
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const bf16x4 lo = lds_read_tr16(vt + 16 * kb * D + voff[0][dt]);
+        const bf16x4 up = lds_read_tr16(vt + 16 * kb * D + voff[1][dt]);
+        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+        oacc[dt] = mfma32(a, pb, oacc[dt]);
       }
     }
+    l_run += rsum;
 
-    if (it + 1 < nt) lstore(buf ^ 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tiles it+1 (V) and it+2 (K) landed
     __syncthreads();
-  }
+    if (has_next) {
+      s_cur[0] = s_next[0];
+      s_cur[1] = s_next[1];
+    }
+  };
+  // B must equal it & 1 at compile time: run each range two tiles at a time
+  auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
+    int it = a;
+    if ((it & 1) && it < e) body(std::integral_constant<int, 1>{}, Mc, it++);
+    for (; it + 1 < e; it += 2) {
+      body(std::integral_constant<int, 0>{}, Mc, it);
+      body(std::integral_constant<int, 1>{}, Mc, it + 1);
+    }
+    if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
+  };
+  run(std::false_type{}, 0, n_full);
+  run(std::true_type{}, n_full, nt);
 
   // ---- end of step: finalise or save the running state -------------------------------
   const float l_tot = pair_sum(l_run);
   if (hs.flags & kLast) {
     const float inv = 1.f / l_tot;
     bf16* orow = (bf16*)p.o + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
-    #pragma unroll
+#pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
-      #pragma unroll
+#pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int d = 32 * dt + 8 * g + 4 * hi;
         u32x2 w = {pack_bf16x2(oacc[dt][4 * g] * inv, oacc[dt][4 * g + 1] * inv),
@@ -238,9 +295,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       }
     if (!hi) p.lse[st_row] = m_run * kLn2 + logf(l_tot);
   } else {
-    #pragma unroll
+#pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
-      #pragma unroll
+#pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 t = {oacc[dt][4 * g], oacc[dt][4 * g + 1], oacc[dt][4 * g + 2], oacc[dt][4 * g + 3]};
         ((f32x4*)acc_tile)[((wave * NDT + dt) * 4 + g) * 64 + lane] = t;
