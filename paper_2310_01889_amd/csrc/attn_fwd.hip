@@ -32,6 +32,7 @@ namespace {
 
 constexpr int kBM = 128, kBN = 64, kThreads = 256;
 constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units)
+constexpr int kPF = 2;       // LDS operand reads issued this many schedule steps ahead
 
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
@@ -46,6 +47,14 @@ __device__ __forceinline__ int swap_bits23(int r) {
 // bit 2 flipped on odd s.  Tiles are filled with direct-to-LDS loads (no registers):
 // lane i of a 1 KB load lands at byte 16 i of its destination, so each lane fetches the
 // logical chunk that the swizzle puts there.
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
 template <int D>
 __device__ __forceinline__ int swz(int r) {
   if constexpr (D == 128) {
@@ -134,17 +143,18 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   // ---- direct-to-LDS staging: each wave fills 16 rows of a tile ---------------------
   // load j of a wave covers rows wave*16 + j*ROWS_PER_LOAD + lane / CPR; the lane's
   // physical chunk is lane % CPR, its logical (global) chunk that ^ swz(row).
-  int goff[LOADS];
+  int goff[LOADS];  // byte offsets from the tile base
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
     const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
-    goff[j] = r * rs + 8 * ((lane % CPR) ^ swz<D>(r));
+    goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
   }
+  // buffer loads with the LDS flag: the tile base is a wave-uniform descriptor, so the
+  // per-tile address update is scalar work; reads past the tile return zero
   auto dload = [&](const bf16* src_tile, bf16* dst_tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j)
-      __builtin_amdgcn_global_load_lds((const void*)(src_tile + goff[j]),
-                                       (lds_void*)(dst_tile + (wave * 16 + j * ROWS_PER_LOAD) * D), 16, 0, 0);
+      buffer_load_lds16(src_tile, kBN * rs * 2, dst_tile + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
   };
   auto load_k = [&](int it, int buf) __attribute__((always_inline)) { dload(kbase + (long long)it * kBN * rs, sK[buf]); };
   auto load_v = [&](int it, int buf) __attribute__((always_inline)) { dload(vbase + (long long)it * kBN * rs, sV[buf]); };
@@ -183,46 +193,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   // ---- pipeline: K runs one tile ahead of V ------------------------------------------
   // While tile it is processed, LDS holds K tiles it, it+1 and V tile it; loads of K tile
   // it+2 (into the buffer of K tile it) and V tile it+1 (into the buffer of V tile it-1)
-  // are in flight.  The scores of tile it+1 are formed on the matrix cores while the
-  // softmax of tile it runs on the vector ALUs.
-  if (nt > 0) {
-    load_k(0, 0);
-    load_v(0, 0);
-    if (nt > 1) load_k(1, 1);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  f32x16 s_cur[2];
-  if (nt > 0) scores(sK[0], s_cur);
-
-  auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
-    constexpr int B = decltype(Bc)::value;     // it & 1
-    constexpr bool MASK = decltype(Mc)::value;  // tile may hold keys after some query
-    if (it + 2 < nt) load_k(it + 2, B);
-    if (it + 1 < nt) load_v(it + 1, B ^ 1);
-    f32x16 s_next[2];
-    const bool has_next = it + 1 < nt;
-    if (has_next) scores(sK[B ^ 1], s_next);
-
-    if (MASK) {
-      const int kpos0 = hs.k_pos0 + it * kBN;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
-          if (kpos > qpos) s_cur[mt][i] = -INFINITY;
-        }
-    }
-    // online softmax, log2 domain; each lane owns one query and the partner lane l^32
-    // holds the other half of its keys.  The running maximum is raised only when a row's
-    // new maximum exceeds it by more than kTau (probabilities then stay below 2^kTau), so
-    // the rescale of the accumulator -- a wave-uniform branch -- is rare.
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s_cur[mt][i]);
+  // are in flight.  One straight-line region per tile issues the scores of tile it+1 on
+  // the matrix cores, the exponentials of tile it on the vector ALUs and O += V P for
+  // tile it, interleaved (sched_group_barrier); the running-max decision for tile it+1
+  // closes the region, so the only branch (the rare rescale) sits between tiles.
+  auto decide_max = [&](float mx) __attribute__((always_inline)) {
     const float mx2 = pair_max(mx) * sl2;
     if (__builtin_amdgcn_ballot_w64(mx2 > m_run + kTau)) {
       const float m_new = fmaxf(m_run, mx2);
@@ -234,21 +209,54 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
         for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
       m_run = m_new;
     }
+  };
+  auto decide = [&](f32x16* sc) __attribute__((always_inline)) {
+    // online softmax, log2 domain; each lane owns one query and the partner lane l^32
+    // holds the other half of its keys.  The running maximum is raised only when a
+    // row's new maximum exceeds it by more than kTau (probabilities then stay below
+    // 2^kTau), so the rescale of the accumulator -- a wave-uniform branch -- is rare.
+    float mx = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[mt][i]);
+    const float mx2 = pair_max(mx) * sl2;
+    if (__builtin_amdgcn_ballot_w64(mx2 > m_run + kTau)) {
+      const float m_new = fmaxf(m_run, mx2);
+      const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
+      m_run = m_new;
+    }
+  };
+  auto mask = [&](f32x16* sc, int it) __attribute__((always_inline)) {
+    const int kpos0 = hs.k_pos0 + it * kBN;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
+        if (kpos > qpos) sc[mt][i] = -INFINITY;
+      }
+  };
+  // P = exp2(s log2e/sqrt(D) - m) in bf16 and O^T += V^T P^T for one tile
+  auto softmax_pv = [&](const f32x16* sc, const bf16* vt) __attribute__((always_inline)) {
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float rsum = 0.f;
-    const bf16* vt = sV[B];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       u32x4 w;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p0 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
-        const float p1 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
+        const float p0 = fast_exp2(fmaf(sc[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
+        const float p1 = fast_exp2(fmaf(sc[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
         rsum += p0 + p1;
         w[j] = pack_bf16x2(p0, p1);
       }
       const bf16x8 pb = __builtin_bit_cast(bf16x8, w);
-      // O^T += V^T P^T for these 16 keys: A operand = V^T via LDS transpose reads
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         const bf16x4 lo = lds_read_tr16(vt + 16 * kb * D + voff[0][dt]);
@@ -258,15 +266,113 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       }
     }
     l_run += rsum;
+  };
 
+  if (nt > 0) {
+    load_k(0, 0);
+    load_v(0, 0);
+    if (nt > 1) load_k(1, 1);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  f32x16 s_cur[2];
+  if (nt > 0) {
+    scores(sK[0], s_cur);
+    if (n_full == 0) mask(s_cur, 0);
+    decide(s_cur);
+  }
+
+  // tile it with a successor; B = it & 1 at compile time, MN: tile it+1 needs the mask.
+  // The region is laid out by hand in 20 steps separated by scheduling fences: step s
+  // issues the LDS reads of the operands kPF steps ahead, the score MFMA s of tile it+1
+  // (s < 16), the O += V P MFMA s-4 of tile it (s >= 4), and a quarter of the exponentials
+  // of one 16-key group of tile it (s < 16; group g is consumed from step 4g + 4 on) or
+  // part of the next row maximum (s >= 16).
+  auto body_sched = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value;
+    constexpr bool MN = decltype(Mc)::value;
+    static_assert(NKK == 8 && NDT == 4, "hand schedule written for D = 128");
+    if (it + 2 < nt) load_k(it + 2, B);
+    load_v(it + 1, B ^ 1);
+    const bf16* kt = sK[B ^ 1];
+    const bf16* vt = sV[B];
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    f32x16 s_next[2];
+    bf16x8 kop[16], vop[16], pb[4];
+    uint32_t w[4][4];
+    float rs2[4] = {0.f, 0.f, 0.f, 0.f};
+    float mxa = -INFINITY, mxb = -INFINITY;
+    auto read_k = [&](auto Sc) __attribute__((always_inline)) {
+      constexpr int S = decltype(Sc)::value;  // score MFMA S: mt = S / 8, kk = S % 8
+      kop[S] = *(const bf16x8*)(kt + 32 * (S / NKK) * D + koff[S % NKK]);
+    };
+    auto read_v = [&](auto Sc) __attribute__((always_inline)) {
+      constexpr int S = decltype(Sc)::value;  // PV MFMA S: kb = S / NDT, dt = S % NDT
+      const bf16x4 lo = lds_read_tr16(vt + 16 * (S / NDT) * D + voff[0][S % NDT]);
+      const bf16x4 up = lds_read_tr16(vt + 16 * (S / NDT) * D + voff[1][S % NDT]);
+      vop[S] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+    };
+    static_for<0, kPF>([&](auto Sc) __attribute__((always_inline)) { read_k(Sc); });
+    static_for<0, 20>([&](auto Sc) __attribute__((always_inline)) {
+      constexpr int S = decltype(Sc)::value;
+      if constexpr (S + kPF < 16) read_k(std::integral_constant<int, S + kPF>{});
+      if constexpr (S + kPF >= 4 && S + kPF < 20) read_v(std::integral_constant<int, S + kPF - 4>{});
+      if constexpr (S < 16) {
+        constexpr int mt = S / NKK, kk = S % NKK;
+        if constexpr (kk == 0) s_next[mt] = f32x16{};
+        s_next[mt] = mfma32(kop[S], qreg[kk], s_next[mt]);
+      }
+      if constexpr (S >= 4) {
+        constexpr int q = S - 4, kb = q / NDT, dt = q % NDT;
+        if constexpr (dt == 0) pb[kb] = __builtin_bit_cast(bf16x8, u32x4{w[kb][0], w[kb][1], w[kb][2], w[kb][3]});
+        oacc[dt] = mfma32(vop[q], pb[kb], oacc[dt]);
+      }
+      if constexpr (S < 16) {
+        constexpr int kb = S / 4, j = S % 4;
+        const float p0 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
+        const float p1 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
+        w[kb][j] = pack_bf16x2(p0, p1);
+        rs2[j] = dot2_bf16_ones(w[kb][j], rs2[j]);  // row sum of the bf16 probabilities used
+      } else if constexpr (S < 18) {
+        if constexpr (S == 16 && MN) mask(s_next, it + 1);
+#pragma unroll
+        for (int i = 8 * (S - 16); i < 8 * (S - 15); ++i) mxa = fmaxf(mxa, s_next[0][i]);
+      } else {
+#pragma unroll
+        for (int i = 8 * (S - 18); i < 8 * (S - 17); ++i) mxb = fmaxf(mxb, s_next[1][i]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    l_run += (rs2[0] + rs2[1]) + (rs2[2] + rs2[3]);
+    decide_max(fmaxf(mxa, mxb));
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tiles it+1 (V) and it+2 (K) landed
     __syncthreads();
-    if (has_next) {
-      s_cur[0] = s_next[0];
-      s_cur[1] = s_next[1];
-    }
+    s_cur[0] = s_next[0];
+    s_cur[1] = s_next[1];
   };
-  // B must equal it & 1 at compile time: run each range two tiles at a time
+  // other head dims: the same work, ordered by the compiler
+  auto body_plain = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value;
+    constexpr bool MN = decltype(Mc)::value;
+    if (it + 2 < nt) load_k(it + 2, B);
+    load_v(it + 1, B ^ 1);
+    f32x16 s_next[2];
+    scores(sK[B ^ 1], s_next);
+    softmax_pv(s_cur, sV[B]);
+    if (MN) mask(s_next, it + 1);
+    decide(s_next);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    s_cur[0] = s_next[0];
+    s_cur[1] = s_next[1];
+  };
+  auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+    if constexpr (D == 128)
+      body_sched(Bc, Mc, it);
+    else
+      body_plain(Bc, Mc, it);
+  };
+  // tiles [a, e) that have successors, two at a time so that B is a constant
   auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
     int it = a;
     if ((it & 1) && it < e) body(std::integral_constant<int, 1>{}, Mc, it++);
@@ -276,8 +382,16 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     }
     if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
   };
-  run(std::false_type{}, 0, n_full);
-  run(std::true_type{}, n_full, nt);
+  if (nt > 0) {
+    const int split = max(0, min(nt - 1, n_full - 1));  // from here on tile it+1 is masked
+    run(std::false_type{}, 0, split);
+    run(std::true_type{}, split, nt - 1);
+    // last tile: no successor
+    if ((nt - 1) & 1)
+      softmax_pv(s_cur, sV[1]);
+    else
+      softmax_pv(s_cur, sV[0]);
+  }
 
   // ---- end of step: finalise or save the running state -------------------------------
   const float l_tot = pair_sum(l_run);

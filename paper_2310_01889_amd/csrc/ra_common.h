@@ -47,6 +47,17 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* lds_ptr) {
   return __builtin_bit_cast(bf16x4, t);
 }
 
+// Direct-to-LDS load of 16 bytes per lane through a buffer descriptor: lane i reads
+// base + voff_bytes (reads at or past num_bytes return zero) and its data lands at byte
+// 16 i of lds_dst, which must be wave-uniform.  The descriptor is scalar, so moving base
+// from tile to tile costs no vector instructions.
+__device__ __forceinline__ void buffer_load_lds16(const void* base, int num_bytes, void* lds_dst, int voff_bytes) {
+#if __HIP_DEVICE_COMPILE__
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, num_bytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)lds_dst, 16, voff_bytes, 0, 0, 0);
+#endif
+}
+
 // Max / sum of a value with the same value in lane l ^ 32 (v_permlane32_swap).
 __device__ __forceinline__ float pair_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
