@@ -161,6 +161,32 @@ int blockwise_linear(const void* x, const void* w, const void* residual, void* y
 int blockwise_linear_bwd(const void* x, const void* w, const void* dy, void* dx, float* dw,
                          int T, int d_in, int d_out, int block, hipStream_t stream);
 
+/*
+ * One transformer layer as Algorithm 1 composes it, bf16, batch 1: the query, key and value
+ * of each host's input block, ring attention over the n_hosts hosts, the output projection
+ * with residual, and the blockwise feed-forward network on each host's block with residual:
+ *     Q, K, V = X Wq, X Wk, X Wv;  A = RingAttention(Q, K, V);  Y = X + A Wo;
+ *     Z = Y + act(Y W1) W2          (no biases, no normalisation, no positional encoding)
+ *   x  in bf16 [S, d_model];  wq, wk, wv, wo in bf16 [d_model, d_model];
+ *   w1 in bf16 [d_model, d_ff]; w2 in bf16 [d_ff, d_model];  z out bf16 [S, d_model]
+ *   Heads: d_model = n_heads * D with D in {64, 128}; head h owns columns [h D, (h+1) D).
+ *   The host block c = S / n_hosts (a multiple of 256) is also the projection / FFN block.
+ */
+int ring_layer_fwd(const void* x, const void* wq, const void* wk, const void* wv, const void* wo,
+                   const void* w1, const void* w2, void* z, int S, int d_model, int n_heads,
+                   int d_ff, int n_hosts, int causal, int act, hipStream_t stream);
+
+/*
+ * Backward of ring_layer_fwd for upstream dz (bf16 [S, d_model]).  Every activation is
+ * recomputed from x (full gradient checkpointing, the paper's training setting).
+ *   dx out bf16 [S, d_model]; dwq, dwk, dwv, dwo out f32 [d_model, d_model];
+ *   dw1 out f32 [d_model, d_ff]; dw2 out f32 [d_ff, d_model] (overwritten).
+ */
+int ring_layer_bwd(const void* x, const void* wq, const void* wk, const void* wv, const void* wo,
+                   const void* w1, const void* w2, const void* dz, void* dx, float* dwq, float* dwk,
+                   float* dwv, float* dwo, float* dw1, float* dw2, int S, int d_model, int n_heads,
+                   int d_ff, int n_hosts, int causal, int act, hipStream_t stream);
+
 /* Description of the last error returned on the calling thread ("" if none).  Valid
  * until the next library call on that thread. */
 const char* ring_attn_last_error(void);

@@ -19,7 +19,8 @@ __all__ = [
     "RingAttnError", "library_path", "load", "exported_symbols",
     "ring_attn_fwd", "ring_attn_bwd", "ring_attn_fwd_f32", "ring_attn_bwd_f32",
     "ring_attn_fwd_host", "ring_attn_fwd_ordered", "blockwise_ffn", "blockwise_ffn_bwd",
-    "blockwise_linear", "blockwise_linear_bwd", "attention_fwd", "attention_bwd",
+    "blockwise_linear", "blockwise_linear_bwd", "ring_layer_fwd", "ring_layer_bwd",
+    "attention_fwd", "attention_bwd",
     "ACT_GELU_ERF", "ACT_RELU", "ACT_GELU_TANH",
 ]
 
@@ -40,6 +41,8 @@ _SIGS = {
     "blockwise_ffn_bwd": [_P] * 10 + [_I] * 5 + [_P],
     "blockwise_linear": [_P] * 4 + [_I] * 4 + [_P],
     "blockwise_linear_bwd": [_P] * 5 + [_I] * 4 + [_P],
+    "ring_layer_fwd": [_P] * 8 + [_I] * 7 + [_P],
+    "ring_layer_bwd": [_P] * 15 + [_I] * 7 + [_P],
 }
 
 
@@ -218,6 +221,26 @@ def blockwise_linear_bwd(x, w, dy, dx, dw, block, stream=None):
     bf = torch.bfloat16
     _call("blockwise_linear_bwd", _ptr(x, bf, "x"), _ptr(w, bf, "w"), _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"),
           _ptr(dw, torch.float32, "dw"), T, di, do, int(block), _stream(stream))
+
+
+def ring_layer_fwd(x, wq, wk, wv, wo, w1, w2, z, n_heads, n_hosts, causal=True, act=ACT_GELU_ERF, stream=None):
+    S, dm = (int(s) for s in x.shape)
+    dff = int(w1.shape[1])
+    bf = torch.bfloat16
+    _call("ring_layer_fwd", _ptr(x, bf, "x"), _ptr(wq, bf, "wq"), _ptr(wk, bf, "wk"), _ptr(wv, bf, "wv"),
+          _ptr(wo, bf, "wo"), _ptr(w1, bf, "w1"), _ptr(w2, bf, "w2"), _ptr(z, bf, "z"), S, dm, int(n_heads), dff,
+          int(n_hosts), int(causal), int(act), _stream(stream))
+
+
+def ring_layer_bwd(x, wq, wk, wv, wo, w1, w2, dz, dx, dwq, dwk, dwv, dwo, dw1, dw2, n_heads, n_hosts, causal=True,
+                   act=ACT_GELU_ERF, stream=None):
+    S, dm = (int(s) for s in x.shape)
+    dff = int(w1.shape[1])
+    bf, f = torch.bfloat16, torch.float32
+    _call("ring_layer_bwd", _ptr(x, bf, "x"), _ptr(wq, bf, "wq"), _ptr(wk, bf, "wk"), _ptr(wv, bf, "wv"),
+          _ptr(wo, bf, "wo"), _ptr(w1, bf, "w1"), _ptr(w2, bf, "w2"), _ptr(dz, bf, "dz"), _ptr(dx, bf, "dx"),
+          _ptr(dwq, f, "dwq"), _ptr(dwk, f, "dwk"), _ptr(dwv, f, "dwv"), _ptr(dwo, f, "dwo"), _ptr(dw1, f, "dw1"),
+          _ptr(dw2, f, "dw2"), S, dm, int(n_heads), dff, int(n_hosts), int(causal), int(act), _stream(stream))
 
 
 # ----------------------------------------------------------------------------------

@@ -7,12 +7,13 @@
 // fused into its epilogue.  The backward pass recomputes each block's pre-activation
 // (gradient checkpointing) and accumulates weight gradients in float32.
 #include "ra_gemm.h"
+#include "ra_ops.h"
 #include "ra_runtime.h"
 #include "ringattn.h"
 
 namespace ra {
 
-static int check_gemm_dims(int T, int d_in, int d_out, int block) {
+int check_gemm_dims(int T, int d_in, int d_out, int block) {
   if (!(T > 0 && d_in > 0 && d_out > 0 && block > 0))
     return set_err(RA_EINVAL, "sizes must be positive (T=%d d_in=%d d_out=%d block=%d)", T, d_in, d_out, block);
   if (T % block) return set_err(RA_EUNSUPPORTED, "T=%d is not a multiple of block=%d", T, block);
@@ -24,24 +25,14 @@ static int check_gemm_dims(int T, int d_in, int d_out, int block) {
   return RA_OK;
 }
 
-static int gemm(const GemmArgs& g, bool ta, bool tb, int epi, hipStream_t st) {
+int gemm(const GemmArgs& g, bool ta, bool tb, int epi, hipStream_t st) {
   RA_HIP(timed_launch(RA_KERNEL_GEMM, st, [&] { return launch_gemm(g, ta, tb, epi, st); }));
   return RA_OK;
 }
 
-}  // namespace ra
-
-using namespace ra;
-
-extern "C" {
-
-int blockwise_ffn(const void* x, const void* w1, const void* b1, const void* w2, const void* b2, void* y, int T,
-                  int d_model, int d_ff, int block, int act, hipStream_t stream) {
-  g_err.clear();
-  if (!x || !w1 || !w2 || !y) return set_err(RA_EINVAL, "null pointer argument");
-  if (act < 0 || act > 2) return set_err(RA_EINVAL, "act=%d is not an ra_act value", act);
-  int rc = check_gemm_dims(T, d_model, d_ff, block);
-  if (rc) return rc;
+int ffn_forward(const void* x, const void* w1, const void* b1, const void* w2, const void* b2, const void* residual,
+                void* y, int T, int d_model, int d_ff, int block, int act, hipStream_t stream) {
+  int rc;
   CallResources R(stream);
   rc = R.alloc((size_t)block * d_ff * 2);
   if (rc) return rc;
@@ -66,6 +57,7 @@ int blockwise_ffn(const void* x, const void* w1, const void* b1, const void* w2,
     dn.B = w2;
     dn.C = (char*)y + (size_t)r0 * d_model * 2;
     dn.bias = b2;
+    dn.residual = residual ? (const char*)residual + (size_t)r0 * d_model * 2 : nullptr;
     dn.lda = d_ff;
     dn.ldb = d_model;
     dn.ldc = d_model;
@@ -78,14 +70,10 @@ int blockwise_ffn(const void* x, const void* w1, const void* b1, const void* w2,
   return RA_OK;
 }
 
-int blockwise_ffn_bwd(const void* x, const void* w1, const void* b1, const void* w2, const void* dy, void* dx,
-                      float* dw1, float* db1, float* dw2, float* db2, int T, int d_model, int d_ff, int block,
-                      int act, hipStream_t stream) {
-  g_err.clear();
-  if (!x || !w1 || !w2 || !dy || !dx || !dw1 || !dw2) return set_err(RA_EINVAL, "null pointer argument");
-  if (act < 0 || act > 2) return set_err(RA_EINVAL, "act=%d is not an ra_act value", act);
-  int rc = check_gemm_dims(T, d_model, d_ff, block);
-  if (rc) return rc;
+int ffn_backward(const void* x, const void* w1, const void* b1, const void* w2, const void* dy, const void* dx_residual,
+                 void* dx, float* dw1, float* db1, float* dw2, float* db2, int T, int d_model, int d_ff, int block,
+                 int act, hipStream_t stream) {
+  int rc;
   const size_t nb = (size_t)block * d_ff;
   const size_t part = colsum_workspace_floats(d_ff > d_model ? d_ff : d_model);
   CallResources R(stream);
@@ -155,6 +143,7 @@ int blockwise_ffn_bwd(const void* x, const void* w1, const void* b1, const void*
     gx.A = dh;
     gx.B = w1;
     gx.C = (char*)dx + (size_t)r0 * d_model * 2;
+    gx.residual = dx_residual ? (const char*)dx_residual + (size_t)r0 * d_model * 2 : nullptr;
     gx.lda = d_ff;
     gx.ldb = d_ff;
     gx.ldc = d_model;
@@ -164,6 +153,33 @@ int blockwise_ffn_bwd(const void* x, const void* w1, const void* b1, const void*
     if ((rc = gemm(gx, false, true, EPI_BF16, stream))) return rc;
   }
   return RA_OK;
+}
+
+}  // namespace ra
+
+using namespace ra;
+
+extern "C" {
+
+int blockwise_ffn(const void* x, const void* w1, const void* b1, const void* w2, const void* b2, void* y, int T,
+                  int d_model, int d_ff, int block, int act, hipStream_t stream) {
+  g_err.clear();
+  if (!x || !w1 || !w2 || !y) return set_err(RA_EINVAL, "null pointer argument");
+  if (act < 0 || act > 2) return set_err(RA_EINVAL, "act=%d is not an ra_act value", act);
+  int rc = check_gemm_dims(T, d_model, d_ff, block);
+  if (rc) return rc;
+  return ffn_forward(x, w1, b1, w2, b2, nullptr, y, T, d_model, d_ff, block, act, stream);
+}
+
+int blockwise_ffn_bwd(const void* x, const void* w1, const void* b1, const void* w2, const void* dy, void* dx,
+                      float* dw1, float* db1, float* dw2, float* db2, int T, int d_model, int d_ff, int block,
+                      int act, hipStream_t stream) {
+  g_err.clear();
+  if (!x || !w1 || !w2 || !dy || !dx || !dw1 || !dw2) return set_err(RA_EINVAL, "null pointer argument");
+  if (act < 0 || act > 2) return set_err(RA_EINVAL, "act=%d is not an ra_act value", act);
+  int rc = check_gemm_dims(T, d_model, d_ff, block);
+  if (rc) return rc;
+  return ffn_backward(x, w1, b1, w2, dy, nullptr, dx, dw1, db1, dw2, db2, T, d_model, d_ff, block, act, stream);
 }
 
 int blockwise_linear(const void* x, const void* w, const void* residual, void* y, int T, int d_in, int d_out,

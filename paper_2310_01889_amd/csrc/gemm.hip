@@ -253,6 +253,7 @@ hipError_t launch_gemm(const GemmArgs& g, bool ta, bool tb, int epi, hipStream_t
   RA_GEMM_CASE(false, true, EPI_BF16)
   RA_GEMM_CASE(false, true, EPI_ACT_GRAD_BF16)
   RA_GEMM_CASE(true, false, EPI_F32)
+  RA_GEMM_CASE(false, true, EPI_F32)
 #undef RA_GEMM_CASE
   return hipErrorInvalidValue;
 }
@@ -270,5 +271,25 @@ hipError_t launch_colsum_bf16(const void* x, float* part, float* out, int M, int
 }
 
 size_t colsum_workspace_floats(int N) { return (size_t)kCS * N; }
+
+namespace {
+__global__ __launch_bounds__(256) void add_cast_kernel(const float* a, const bf16* b, bf16* out, long long n) {
+  const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i + 3 < n) {
+    const f32x4 x = *(const f32x4*)(a + i);
+    const bf16x4 y = *(const bf16x4*)(b + i);
+    *(u32x2*)(out + i) = u32x2{pack_bf16x2(x[0] + (float)y[0], x[1] + (float)y[1]),
+                               pack_bf16x2(x[2] + (float)y[2], x[3] + (float)y[3])};
+  } else {
+    for (long long j = i; j < n; ++j) out[j] = (bf16)(a[j] + (float)b[j]);
+  }
+}
+}  // namespace
+
+hipError_t launch_add_cast_bf16(const float* a, const void* b, void* out, long long n, hipStream_t st) {
+  const long long blocks = (n / 4 + 255) / 256 + 1;
+  hipLaunchKernelGGL(add_cast_kernel, dim3(blocks), dim3(256), 0, st, a, (const bf16*)b, (bf16*)out, n);
+  return hipGetLastError();
+}
 
 }  // namespace ra

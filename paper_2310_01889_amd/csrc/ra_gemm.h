@@ -36,4 +36,7 @@ hipError_t launch_colsum_bf16(const void* x, float* part, float* out, int M, int
                               hipStream_t st);
 size_t colsum_workspace_floats(int N);
 
+// out = bf16(a + b) elementwise for float32 a and bf16 b (n elements).
+hipError_t launch_add_cast_bf16(const float* a, const void* b, void* out, long long n, hipStream_t st);
+
 }  // namespace ra
