@@ -169,6 +169,31 @@ def main():
         f5 = 4.0 * H5 * D * host_pairs(c5, 7, N5)
         extra["host7_of_8_c32768_H32"] = {"ms": round(ms5, 3), "tflops": round(f5 / ms5 / 1e9, 2),
                                           "query_tokens_per_s": round(c5 / (ms5 * 1e-3), 1)}
+        del qb, k5, v5, ob, lb
+        # blockwise FFN and the full layer (forward + backward) at d_model 4096, d_ff 16384,
+        # S = 65536 in 8 host blocks of 8192, 32 heads of 128
+        S4, dm, dff, H4, N4 = 65536, 4096, 16384, 32, 8
+        w = lambda *shape: (torch.randn(*shape, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+        x4, dz4 = mk(S4, dm), mk(S4, dm)
+        wq, wk, wv, wo = (w(dm, dm) for _ in range(4))
+        w1, w2 = w(dm, dff), w(dff, dm)
+        y4 = torch.empty_like(x4)
+        msf, _ = time_calls(lambda: ra.blockwise_ffn(x4, w1, None, w2, None, y4, S4 // N4), 3, 1)
+        fffn = 2.0 * 2 * S4 * dm * dff
+        extra["ffn_fwd_T65536_d4096_ff16384"] = {"ms": round(msf, 3), "tflops": round(fffn / msf / 1e9, 2)}
+        z4, dx4 = torch.empty_like(x4), torch.empty_like(x4)
+        f32 = lambda *shape: torch.empty(*shape, dtype=torch.float32, device="cuda")
+        dws = [f32(dm, dm) for _ in range(4)] + [f32(dm, dff), f32(dff, dm)]
+
+        def layer():
+            ra.ring_layer_fwd(x4, wq, wk, wv, wo, w1, w2, z4, H4, N4, True)
+            ra.ring_layer_bwd(x4, wq, wk, wv, wo, w1, w2, dz4, dx4, *dws, H4, N4, True)
+        msl, _ = time_calls(layer, 2, 1)
+        fatt = 4.0 * H4 * 128 * causal_pairs(S4)
+        flayer = 3.5 * fatt + 3 * 24.0 * S4 * dm * dm  # attention fwd+bwd, GEMMs fwd (24 S h^2) + bwd (2x)
+        extra["layer_fwd_bwd_S65536_d4096"] = {"ms": round(msl, 3), "tflops": round(flayer / msl / 1e9, 2),
+                                               "tokens_per_s": round(S4 / (msl * 1e-3), 1),
+                                               "note": "algorithmic flops; backward recomputes the forward"}
         out["extra"] = extra
 
     if not args.no_cpu:
