@@ -15,16 +15,13 @@
 namespace ra {
 namespace {
 
-__device__ __forceinline__ int swap_bits23(int r) {
-  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
-}
 
 // -------------------------------------------------------------------------------------
 // Delta_r = sum_d dO_rd * O_rd  (float32 [B, H, S]); rows in memory order (b, r, h).
 // -------------------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const bf16* dO, float* delta,
-                                                           int B, int S, int H) {
+__global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const bf16* dO, const float* lse,
+                                                           float* delta, float* lse2, int B, int S, int H) {
   constexpr int TPR = D / 8;  // threads per row
   const long long row = (long long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
   const int c = (threadIdx.x % TPR) * 8;
@@ -41,7 +38,9 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const 
     const int h = (int)(row % H);
     const long long br = row / H;
     const int r = (int)(br % S), b = (int)(br / S);
-    delta[((long long)b * H + h) * S + r] = s;
+    const long long idx = ((long long)b * H + h) * S + r;
+    delta[idx] = s;
+    lse2[idx] = lse[idx] * kLog2e;  // the bf16 step kernels work in log2 units
   }
 }
 
@@ -70,26 +69,27 @@ __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const 
 
 // =====================================================================================
 // bf16 dK/dV kernel: 4 waves x 32 keys = 128 keys per workgroup; loops over 64-query
-// tiles of the host's block staged in LDS.  Per wave:
-//   S  = Q K^T   [query x key], lanes run over keys (A = Q rows from LDS, with row bits
-//                2 and 3 swapped; B = K of the wave's keys held in registers)
-//   P  = exp2(S * log2e/sqrt(D) - lse * log2e), masked -> 0
-//   dV^T += dO^T P     (A = dO^T by LDS transpose read, B = P from registers)
-//   dP = dO V^T        (A = dO rows, B = V of the wave's keys in registers)
-//   dS = P * (dP - Delta)
-//   dK^T += Q^T dS     (A = Q^T by LDS transpose read, B = dS)
+// tiles of the host's block.  Per wave, lanes run over the wave's keys:
+//   S  = Q K^T            [query x key] (A = Q rows from LDS with row bits 2 and 3
+//                          swapped, B = K of the wave's keys held in registers)
+//   P  = exp2(S log2e/sqrt(D) - lse log2e)                       (masked -> 0)
+//   dP = dO V^T - Delta   (A = dO rows, B = V in registers; starts at -Delta)
+//   dS = P * dP
+//   dV^T += dO^T P        (A = dO^T by LDS transpose read, B = P)
+//   dK^T += Q^T dS        (A = Q^T by LDS transpose read, B = dS)
+// Q and dO tiles (XOR-swizzled rows) and the tile's lse*log2e and Delta are filled by
+// direct-to-LDS buffer loads, double buffered.
 // =====================================================================================
 constexpr int kKB = 128, kQB = 64, kBT = 256;
 
 template <int D>
 __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) {
-  constexpr int QS = D + 8;    // LDS row stride for Q and dO tiles
-  constexpr int NKK = D / 16, NDT = D / 32;
-  constexpr int CPR = D / 8, RPP = kBT / CPR, NPASS = kQB / RPP;
-  __shared__ __attribute__((aligned(16))) bf16 sQ[2][kQB * QS];
-  __shared__ __attribute__((aligned(16))) bf16 sO[2][kQB * QS];  // dO tile
-  __shared__ __attribute__((aligned(16))) float sL[2][kQB];       // lse * log2e
-  __shared__ __attribute__((aligned(16))) float sD[2][kQB];       // Delta
+  constexpr int NKK = D / 16, NDT = D / 32, CPR = D / 8;
+  constexpr int ROWS_PER_LOAD = 64 / CPR, LOADS = kQB / 4 / ROWS_PER_LOAD;
+  __shared__ __attribute__((aligned(1024))) bf16 sQ[2][kQB * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sO[2][kQB * D];  // dO tile
+  __shared__ __attribute__((aligned(256))) float sL[2][kQB];       // lse * log2e
+  __shared__ __attribute__((aligned(256))) float sD[2][kQB];       // Delta
 
   const int n_kt = p.c / kKB;
   const int BH = p.B * p.H;
@@ -102,179 +102,164 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int rs = p.H * D;
 
-  const int key_in_blk = kt * kKB + wave * 32 + l32;  // this lane's key (as B-operand column)
+  const int key_in_blk = kt * kKB + wave * 32 + l32;  // this lane's key (B-operand column)
   const int kpos = hs.k_pos0 + key_in_blk;
   const bf16* krow = (const bf16*)hs.k + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
   const bf16* vrow = (const bf16*)hs.v + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
   bf16x8 kreg[NKK], vreg[NKK];
-  #pragma unroll
+#pragma unroll
   for (int kk = 0; kk < NKK; ++kk) {
     kreg[kk] = *(const bf16x8*)(krow + 16 * kk + 8 * hi);
     vreg[kk] = *(const bf16x8*)(vrow + 16 * kk + 8 * hi);
   }
   f32x16 dkacc[NDT], dvacc[NDT];
-  #pragma unroll
+#pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
-    #pragma unroll
+#pragma unroll
     for (int i = 0; i < 16; ++i) dkacc[dt][i] = dvacc[dt][i] = 0.f;
 
-  // query tiles with at least one query that sees a key of this workgroup
+  // query tiles with at least one query that sees a key of this workgroup; from
+  // qt_free on every query sees every key (no mask)
   const int wg_first_k = hs.k_pos0 + kt * kKB;
-  int qt0 = 0;
   const int n_qtiles = p.c / kQB;
+  int qt0 = 0, qt_free = 0;
   if (p.causal) {
-    // first query position >= wg_first_k
     const int rel = wg_first_k - hs.q_pos0;
     qt0 = rel <= 0 ? 0 : min(n_qtiles, rel / kQB);
+    const int rel_last = wg_first_k + kKB - 1 - hs.q_pos0;  // last key's offset in the q block
+    qt_free = rel_last < 0 ? 0 : min(n_qtiles, (rel_last + kQB - 1) / kQB);
+    qt_free = max(qt_free, qt0);
   }
 
   const bf16* qbase = (const bf16*)p.q + (long long)b * p.q_bstride + h * D;
   const bf16* obase = (const bf16*)p.dO + (long long)b * p.q_bstride + h * D;
   const long long lrow0 = (long long)bh * p.Sq + hs.q_row0;
-  const int st_r = tid / CPR, st_c = (tid % CPR) * 8;
-  u32x4 qpre[NPASS], opre[NPASS];
-  float lpre = 0.f, dpre = 0.f;
-  auto gload = [&](int qt) {
-    #pragma unroll
-    for (int ps = 0; ps < NPASS; ++ps) {
-      const long long off = (long long)(hs.q_row0 + qt * kQB + st_r + ps * RPP) * rs + st_c;
-      qpre[ps] = *(const u32x4*)(qbase + off);
-      opre[ps] = *(const u32x4*)(obase + off);
+  int goff[LOADS];
+#pragma unroll
+  for (int j = 0; j < LOADS; ++j) {
+    const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
+    goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
+  }
+  auto load_tile = [&](int qt, int buf) __attribute__((always_inline)) {
+    const long long t0 = (long long)(hs.q_row0 + qt * kQB) * rs;
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      buffer_load_lds16(qbase + t0, kQB * rs * 2, &sQ[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
+      buffer_load_lds16(obase + t0, kQB * rs * 2, &sO[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
     }
-    if (tid < kQB) {
-      lpre = p.lse[lrow0 + qt * kQB + tid] * kLog2e;
-      dpre = p.delta[lrow0 + qt * kQB + tid];
-    }
+    if (wave == 0) buffer_load_lds4(p.lse + lrow0 + qt * kQB, kQB * 4, sL[buf], 4 * lane);
+    if (wave == 1) buffer_load_lds4(p.delta + lrow0 + qt * kQB, kQB * 4, sD[buf], 4 * lane);
   };
-  auto lstore = [&](int buf) {
-    #pragma unroll
-    for (int ps = 0; ps < NPASS; ++ps) {
-      const int r = st_r + ps * RPP;
-      *(u32x4*)(&sQ[buf][r * QS + st_c]) = qpre[ps];
-      *(u32x4*)(&sO[buf][r * QS + st_c]) = opre[ps];
+  const int qrow = swap_bits23(l32);
+  int roff[NKK];
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk) roff[kk] = qrow * D + 8 * ((2 * kk + hi) ^ swz<D>(qrow));
+  const int g16 = lane >> 4, li = lane & 15;
+  int toff[2][NDT];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const int row = 8 * hi + 4 * r + (li >> 2);
+      const int d = 32 * dt + 16 * (g16 & 1) + 4 * (li & 3);
+      toff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
-    if (tid < kQB) {
-      sL[buf][tid] = lpre;
-      sD[buf][tid] = dpre;
-    }
-  };
-
   const float sl2 = p.scale * kLog2e;
-  const int prow = swap_bits23(l32);
-  if (qt0 < n_qtiles) {
-    gload(qt0);
-    lstore(0);
-  }
-  __syncthreads();
-  for (int qt = qt0; qt < n_qtiles; ++qt) {
-    const int buf = (qt - qt0) & 1;
-    if (qt + 1 < n_qtiles) gload(qt + 1);
-    const int qpos0 = hs.q_pos0 + qt * kQB;
 
-    // S = Q K^T : two 32-query tiles
-    f32x16 sacc[2];
-    #pragma unroll
+  auto body = [&](auto Bc, auto Mc, int qt) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value;
+    constexpr bool MASK = decltype(Mc)::value;
+    if (qt + 1 < n_qtiles) load_tile(qt + 1, B ^ 1);
+    const bf16* qtl = sQ[B];
+    const bf16* otl = sO[B];
+    const int qpos0 = hs.q_pos0 + qt * kQB;
+    // S and dP (rows = queries 32 qm + 16 (i/8) + 8 hi + i%8 of the tile)
+    f32x16 sacc[2], dpacc[2];
+#pragma unroll
     for (int qm = 0; qm < 2; ++qm) {
-      #pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[qm][i] = 0.f;
-      const bf16* qr = &sQ[buf][(32 * qm + prow) * QS + 8 * hi];
-      #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) sacc[qm] = mfma32(*(const bf16x8*)(qr + 16 * kk), kreg[kk], sacc[qm]);
-    }
-    // P (queries 32qm + 16(i/8) + 8hi + i%8 of the tile)
-    const bool need_mask = p.causal && (wg_first_k + kKB - 1 > qpos0);
-    #pragma unroll
-    for (int qm = 0; qm < 2; ++qm)
-      #pragma unroll
+#pragma unroll
       for (int hb = 0; hb < 2; ++hb) {
         const int q0 = 32 * qm + 16 * hb + 8 * hi;
-        const f32x4 la = *(const f32x4*)&sL[buf][q0];
-        const f32x4 lb = *(const f32x4*)&sL[buf][q0 + 4];
-        #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float lv = e < 4 ? la[e] : lb[e - 4];
-          float pv = fast_exp2(fmaf(sacc[qm][8 * hb + e], sl2, -lv));
-          if (need_mask && kpos > qpos0 + q0 + e) pv = 0.f;
-          sacc[qm][8 * hb + e] = pv;
+        const f32x4 da = *(const f32x4*)&sD[B][q0];
+        const f32x4 db = *(const f32x4*)&sD[B][q0 + 4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          dpacc[qm][8 * hb + e] = -da[e];
+          dpacc[qm][8 * hb + 4 + e] = -db[e];
+          sacc[qm][8 * hb + e] = 0.f;
+          sacc[qm][8 * hb + 4 + e] = 0.f;
         }
       }
-    // dV^T += dO^T P
-    bf16x8 pb[4];
-    #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      u32x4 w;
-      #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        w[j] = pack_bf16x2(sacc[kb >> 1][8 * (kb & 1) + 2 * j], sacc[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
-      pb[kb] = __builtin_bit_cast(bf16x8, w);
-    }
-    const int g = lane >> 4, li = lane & 15;
-    const int tcol = 16 * (g & 1) + 4 * (li & 3);
-    const int trow = 8 * hi + (li >> 2);
-    #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const bf16* op = &sO[buf][(16 * kb + trow) * QS + tcol];
-      #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x4 lo = lds_read_tr16(op + 32 * dt);
-        const bf16x4 up = lds_read_tr16(op + 4 * QS + 32 * dt);
-        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-        dvacc[dt] = mfma32(a, pb[kb], dvacc[dt]);
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) {
+        sacc[qm] = mfma32(*(const bf16x8*)(qtl + 32 * qm * D + roff[kk]), kreg[kk], sacc[qm]);
+        dpacc[qm] = mfma32(*(const bf16x8*)(otl + 32 * qm * D + roff[kk]), vreg[kk], dpacc[qm]);
       }
     }
-    // dP = dO V^T, then dS = P * (dP - Delta)
-    #pragma unroll
-    for (int qm = 0; qm < 2; ++qm) {
-      f32x16 dp;
-      #pragma unroll
-      for (int i = 0; i < 16; ++i) dp[i] = 0.f;
-      const bf16* orr = &sO[buf][(32 * qm + prow) * QS + 8 * hi];
-      #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) dp = mfma32(*(const bf16x8*)(orr + 16 * kk), vreg[kk], dp);
-      #pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        const int q0 = 32 * qm + 16 * hb + 8 * hi;
-        const f32x4 da = *(const f32x4*)&sD[buf][q0];
-        const f32x4 db = *(const f32x4*)&sD[buf][q0 + 4];
-        #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float dv = e < 4 ? da[e] : db[e - 4];
-          sacc[qm][8 * hb + e] = sacc[qm][8 * hb + e] * (dp[8 * hb + e] - dv);
+    // P, dS (bf16) and the two transposed products, 16 queries at a time
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const int qm = kb >> 1, hb = kb & 1;
+      const int q0 = 32 * qm + 16 * hb + 8 * hi;
+      const f32x4 la = *(const f32x4*)&sL[B][q0];
+      const f32x4 lb = *(const f32x4*)&sL[B][q0 + 4];
+      u32x4 wp, ws;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float pv[2], dsv[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int ee = 2 * j + e;
+          const float lv = ee < 4 ? la[ee] : lb[ee - 4];
+          float pr = fast_exp2(fmaf(sacc[qm][8 * hb + ee], sl2, -lv));
+          if (MASK && kpos > qpos0 + q0 + ee) pr = 0.f;
+          pv[e] = pr;
+          dsv[e] = pr * dpacc[qm][8 * hb + ee];
         }
+        wp[j] = pack_bf16x2(pv[0], pv[1]);
+        ws[j] = pack_bf16x2(dsv[0], dsv[1]);
       }
-    }
-    // dK^T += Q^T dS
-    #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      u32x4 w;
-      #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        w[j] = pack_bf16x2(sacc[kb >> 1][8 * (kb & 1) + 2 * j], sacc[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
-      const bf16x8 dsb = __builtin_bit_cast(bf16x8, w);
-      const bf16* qp = &sQ[buf][(16 * kb + trow) * QS + tcol];
-      #pragma unroll
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, wp);
+      const bf16x8 dsb = __builtin_bit_cast(bf16x8, ws);
+#pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x4 lo = lds_read_tr16(qp + 32 * dt);
-        const bf16x4 up = lds_read_tr16(qp + 4 * QS + 32 * dt);
-        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-        dkacc[dt] = mfma32(a, dsb, dkacc[dt]);
+        const bf16x4 olo = lds_read_tr16(otl + 16 * kb * D + toff[0][dt]);
+        const bf16x4 oup = lds_read_tr16(otl + 16 * kb * D + toff[1][dt]);
+        dvacc[dt] = mfma32(bf16x8{olo[0], olo[1], olo[2], olo[3], oup[0], oup[1], oup[2], oup[3]}, pb, dvacc[dt]);
+        const bf16x4 qlo = lds_read_tr16(qtl + 16 * kb * D + toff[0][dt]);
+        const bf16x4 qup = lds_read_tr16(qtl + 16 * kb * D + toff[1][dt]);
+        dkacc[dt] = mfma32(bf16x8{qlo[0], qlo[1], qlo[2], qlo[3], qup[0], qup[1], qup[2], qup[3]}, dsb, dkacc[dt]);
       }
     }
-    if (qt + 1 < n_qtiles) lstore(buf ^ 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-  }
+  };
+  auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
+    int it = a;
+    if (((it - qt0) & 1) && it < e) body(std::integral_constant<int, 1>{}, Mc, it++);
+    for (; it + 1 < e; it += 2) {
+      body(std::integral_constant<int, 0>{}, Mc, it);
+      body(std::integral_constant<int, 1>{}, Mc, it + 1);
+    }
+    if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
+  };
+  if (qt0 < n_qtiles) load_tile(qt0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  run(std::true_type{}, qt0, qt_free);
+  run(std::false_type{}, qt_free, n_qtiles);
 
   // add into the float32 gradient of the block (its home rows)
   const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key_in_blk) * rs + h * D;
-  #pragma unroll
+#pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
-    #pragma unroll
+#pragma unroll
     for (int gg = 0; gg < 4; ++gg) {
       const int d = 32 * dt + 8 * gg + 4 * hi;
       f32x4* dkp = (f32x4*)(p.dk + grow + d);
       f32x4* dvp = (f32x4*)(p.dv + grow + d);
       f32x4 k4 = *dkp, v4 = *dvp;
-      #pragma unroll
+#pragma unroll
       for (int e = 0; e < 4; ++e) {
         k4[e] += dkacc[dt][4 * gg + e] * p.scale;
         v4[e] += dvacc[dt][4 * gg + e];
@@ -286,22 +271,23 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
 
 // =====================================================================================
 // bf16 dQ kernel: 4 waves x 32 queries = 128 queries per workgroup; loops over 64-key
-// tiles.  Per wave, lanes run over queries:
-//   S^T = K Q^T (A = K rows from LDS with bits 2,3 swapped, B = Q in registers)
-//   P^T = exp2(S^T * log2e/sqrt(D) - lse*log2e)
-//   dP^T = V dO^T (A = V rows, B = dO in registers)
-//   dS^T = P^T * (dP^T - Delta)
-//   dQ^T += K^T dS^T (A = K^T by LDS transpose read, B = dS^T)
+// tiles of the block.  Per wave, lanes run over queries:
+//   S^T  = K Q^T            (A = K rows from LDS, B = Q in registers)
+//   dP^T = V dO^T - Delta   (A = V rows, B = dO in registers; the accumulator starts at
+//                            -Delta of the lane's query, so the subtraction is free)
+//   P^T  = exp2(S^T log2e/sqrt(D) - lse log2e),  dS^T = P^T * dP^T   (masked -> 0)
+//   dQ^T += K^T dS^T        (A = K^T by LDS transpose read, B = dS^T)
+// K and V tiles are filled by direct-to-LDS buffer loads into XOR-swizzled unpadded rows
+// (see swz), double buffered: tile it+1 streams in while tile it is processed.
 // =====================================================================================
 constexpr int kQQ = 128, kKK = 64;
 
 template <int D>
-__global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
-  constexpr int KS = D + 8;
-  constexpr int NKK = D / 16, NDT = D / 32;
-  constexpr int CPR = D / 8, RPP = kBT / CPR, NPASS = kKK / RPP;
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][kKK * KS];
-  __shared__ __attribute__((aligned(16))) bf16 sV[2][kKK * KS];
+__global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
+  constexpr int NKK = D / 16, NDT = D / 32, CPR = D / 8;
+  constexpr int ROWS_PER_LOAD = 64 / CPR, LOADS = kKK / 4 / ROWS_PER_LOAD;
+  __shared__ __attribute__((aligned(1024))) bf16 sK[2][kKK * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV[2][kKK * D];
 
   const int n_qt = p.c / kQQ;
   const int BH = p.B * p.H;
@@ -319,124 +305,143 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dq_bf16_kernel(const BwdStep p) {
   const int qpos = hs.q_pos0 + qt * kQQ + wave * 32 + l32;
   const int tile_first_q = hs.q_pos0 + qt * kQQ;
   const long long lrow = (long long)bh * p.Sq + qr;
-  const float lse2 = p.lse[lrow] * kLog2e;
+  const float lse2 = p.lse[lrow];  // lse * log2e (written by the preprocess kernel)
   const float dlt = p.delta[lrow];
 
   bf16x8 qreg[NKK], oreg[NKK];
   {
     const long long off = (long long)b * p.q_bstride + (long long)qr * rs + h * D + 8 * hi;
-    #pragma unroll
+#pragma unroll
     for (int kk = 0; kk < NKK; ++kk) {
       qreg[kk] = *(const bf16x8*)((const bf16*)p.q + off + 16 * kk);
       oreg[kk] = *(const bf16x8*)((const bf16*)p.dO + off + 16 * kk);
     }
   }
   f32x16 dqacc[NDT];
-  #pragma unroll
+#pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
-    #pragma unroll
+#pragma unroll
     for (int i = 0; i < 16; ++i) dqacc[dt][i] = 0.f;
 
-  int nt = p.c / kKK;
+  int nt = p.c / kKK, n_full = nt;
   if (p.causal) {
     const int vis = tile_first_q + kQQ - hs.k_pos0;
     nt = min(nt, max(0, (vis + kKK - 1) / kKK));
+    n_full = min(nt, max(0, (tile_first_q - hs.k_pos0 + 1) / kKK));
   }
   const bf16* kbase = (const bf16*)hs.k + (long long)b * hs.kv_bstride + h * D;
   const bf16* vbase = (const bf16*)hs.v + (long long)b * hs.kv_bstride + h * D;
-  const int st_r = tid / CPR, st_c = (tid % CPR) * 8;
-  u32x4 kpre[NPASS], vpre[NPASS];
-  auto gload = [&](int it) {
-    #pragma unroll
-    for (int ps = 0; ps < NPASS; ++ps) {
-      const long long off = (long long)(it * kKK + st_r + ps * RPP) * rs + st_c;
-      kpre[ps] = *(const u32x4*)(kbase + off);
-      vpre[ps] = *(const u32x4*)(vbase + off);
-    }
-  };
-  auto lstore = [&](int buf) {
-    #pragma unroll
-    for (int ps = 0; ps < NPASS; ++ps) {
-      const int r = st_r + ps * RPP;
-      *(u32x4*)(&sK[buf][r * KS + st_c]) = kpre[ps];
-      *(u32x4*)(&sV[buf][r * KS + st_c]) = vpre[ps];
-    }
-  };
-  const float sl2 = p.scale * kLog2e;
-  const int krow_perm = swap_bits23(l32);
-  if (nt > 0) {
-    gload(0);
-    lstore(0);
+
+  // direct-to-LDS staging: load j of a wave fills rows wave*16 + j*ROWS_PER_LOAD + lane/CPR
+  int goff[LOADS];
+#pragma unroll
+  for (int j = 0; j < LOADS; ++j) {
+    const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
+    goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
   }
-  __syncthreads();
-  for (int it = 0; it < nt; ++it) {
-    const int buf = it & 1;
-    if (it + 1 < nt) gload(it + 1);
+  auto load_tile = [&](int it, int buf) __attribute__((always_inline)) {
+    const long long t0 = (long long)it * kKK * rs;
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+      buffer_load_lds16(kbase + t0, kKK * rs * 2, &sK[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
+      buffer_load_lds16(vbase + t0, kKK * rs * 2, &sV[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
+    }
+  };
+  // row reads (A operand, rows 32 mt + swap_bits23(l32)) and transpose reads of the tiles
+  const int krow = swap_bits23(l32);
+  int roff[NKK];
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk) roff[kk] = krow * D + 8 * ((2 * kk + hi) ^ swz<D>(krow));
+  const int g16 = lane >> 4, li = lane & 15;
+  int toff[2][NDT];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const int row = 8 * hi + 4 * r + (li >> 2);
+      const int d = 32 * dt + 16 * (g16 & 1) + 4 * (li & 3);
+      toff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
+    }
+  const float sl2 = p.scale * kLog2e;
+
+  auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value;
+    constexpr bool MASK = decltype(Mc)::value;
+    if (it + 1 < nt) load_tile(it + 1, B ^ 1);
+    const bf16* kt = sK[B];
+    const bf16* vt = sV[B];
     f32x16 sacc[2], dpacc[2];
-    #pragma unroll
+#pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      #pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[mt][i] = dpacc[mt][i] = 0.f;
-      const bf16* kr = &sK[buf][(32 * mt + krow_perm) * KS + 8 * hi];
-      const bf16* vr = &sV[buf][(32 * mt + krow_perm) * KS + 8 * hi];
-      #pragma unroll
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        sacc[mt][i] = 0.f;
+        dpacc[mt][i] = -dlt;
+      }
+#pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
-        sacc[mt] = mfma32(*(const bf16x8*)(kr + 16 * kk), qreg[kk], sacc[mt]);
-        dpacc[mt] = mfma32(*(const bf16x8*)(vr + 16 * kk), oreg[kk], dpacc[mt]);
+        sacc[mt] = mfma32(*(const bf16x8*)(kt + 32 * mt * D + roff[kk]), qreg[kk], sacc[mt]);
+        dpacc[mt] = mfma32(*(const bf16x8*)(vt + 32 * mt * D + roff[kk]), oreg[kk], dpacc[mt]);
       }
     }
     const int kpos0 = hs.k_pos0 + it * kKK;
-    const bool need_mask = p.causal && (kpos0 + kKK - 1 > tile_first_q);
-    bf16x8 dsb[4];
-    #pragma unroll
+#pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       u32x4 w;
-      #pragma unroll
+#pragma unroll
       for (int j = 0; j < 4; ++j) {
         float ds2[2];
-        #pragma unroll
+#pragma unroll
         for (int e = 0; e < 2; ++e) {
           const int i = 8 * (kb & 1) + 2 * j + e;
           const int mt = kb >> 1;
           float pv = fast_exp2(fmaf(sacc[mt][i], sl2, -lse2));
-          if (need_mask) {
+          if (MASK) {
             const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
             if (kpos > qpos) pv = 0.f;
           }
-          ds2[e] = pv * (dpacc[mt][i] - dlt);
+          ds2[e] = pv * dpacc[mt][i];
         }
         w[j] = pack_bf16x2(ds2[0], ds2[1]);
       }
-      dsb[kb] = __builtin_bit_cast(bf16x8, w);
-    }
-    // dQ^T += K^T dS^T
-    const int g = lane >> 4, li = lane & 15;
-    const int tcol = 16 * (g & 1) + 4 * (li & 3);
-    const int trow = 8 * hi + (li >> 2);
-    #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const bf16* kp = &sK[buf][(16 * kb + trow) * KS + tcol];
-      #pragma unroll
+      const bf16x8 dsb = __builtin_bit_cast(bf16x8, w);
+      // dQ^T += K^T dS^T for these 16 keys
+#pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x4 lo = lds_read_tr16(kp + 32 * dt);
-        const bf16x4 up = lds_read_tr16(kp + 4 * KS + 32 * dt);
+        const bf16x4 lo = lds_read_tr16(kt + 16 * kb * D + toff[0][dt]);
+        const bf16x4 up = lds_read_tr16(kt + 16 * kb * D + toff[1][dt]);
         const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-        dqacc[dt] = mfma32(a, dsb[kb], dqacc[dt]);
+        dqacc[dt] = mfma32(a, dsb, dqacc[dt]);
       }
     }
-    if (it + 1 < nt) lstore(buf ^ 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-  }
+  };
+  auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
+    int it = a;
+    if ((it & 1) && it < e) body(std::integral_constant<int, 1>{}, Mc, it++);
+    for (; it + 1 < e; it += 2) {
+      body(std::integral_constant<int, 0>{}, Mc, it);
+      body(std::integral_constant<int, 1>{}, Mc, it + 1);
+    }
+    if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
+  };
+  if (nt > 0) load_tile(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  run(std::false_type{}, 0, n_full);
+  run(std::true_type{}, n_full, nt);
+
   // dq (float32, [B, Sq, H, D]) += scale * dQ
   float* dqrow = p.dq + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
-  #pragma unroll
+#pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
-    #pragma unroll
+#pragma unroll
     for (int gg = 0; gg < 4; ++gg) {
       const int d = 32 * dt + 8 * gg + 4 * hi;
       f32x4* dp = (f32x4*)(dqrow + d);
       f32x4 t = *dp;
-      #pragma unroll
+#pragma unroll
       for (int e = 0; e < 4; ++e) t[e] += dqacc[dt][4 * gg + e] * p.scale;
       *dp = t;
     }
@@ -593,15 +598,15 @@ __global__ void zero_f32_kernel(float* p, long long n) {
 
 }  // namespace
 
-hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, float* delta, int B, int S, int H, int D,
-                               hipStream_t st) {
+hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, float* delta, float* lse2, int B,
+                               int S, int H, int D, hipStream_t st) {
   const long long rows = (long long)B * S * H;
   const int rpb = 256 / (D / 8);
   const long long blocks = (rows + rpb - 1) / rpb;
   if (D == 128)
-    hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, delta, B, S, H);
+    hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, lse2, B, S, H);
   else
-    hipLaunchKernelGGL(bwd_pre_bf16_kernel<64>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, delta, B, S, H);
+    hipLaunchKernelGGL(bwd_pre_bf16_kernel<64>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, lse2, B, S, H);
   return hipGetLastError();
 }
 

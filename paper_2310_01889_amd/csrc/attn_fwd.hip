@@ -34,9 +34,6 @@ constexpr int kBM = 128, kBN = 64, kThreads = 256;
 constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units)
 constexpr int kPF = 2;       // LDS operand reads issued this many schedule steps ahead
 
-__device__ __forceinline__ int swap_bits23(int r) {
-  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
-}
 
 // LDS tiles are unpadded [64 rows][D] with the 16-byte chunks of each row permuted by
 // an XOR swizzle, so that every read pattern below is free of bank conflicts:
@@ -47,24 +44,6 @@ __device__ __forceinline__ int swap_bits23(int r) {
 // bit 2 flipped on odd s.  Tiles are filled with direct-to-LDS loads (no registers):
 // lane i of a 1 KB load lands at byte 16 i of its destination, so each lane fetches the
 // logical chunk that the swizzle puts there.
-template <int I, int N, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (I < N) {
-    f(std::integral_constant<int, I>{});
-    static_for<I + 1, N>(f);
-  }
-}
-
-template <int D>
-__device__ __forceinline__ int swz(int r) {
-  if constexpr (D == 128) {
-    return 4 * (r & 3) + ((r >> 2) & 3);
-  } else {
-    const int s = (r >> 1) & 7;
-    return s ^ ((s & 1) << 2);
-  }
-}
-
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) {
   constexpr int NKK = D / 16;  // 16-wide reduction steps of q.k

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace ra {
 
 typedef __bf16 bf16;
@@ -58,6 +60,14 @@ __device__ __forceinline__ void buffer_load_lds16(const void* base, int num_byte
 #endif
 }
 
+// As buffer_load_lds16 with 4 bytes per lane (lane i lands at byte 4 i of lds_dst).
+__device__ __forceinline__ void buffer_load_lds4(const void* base, int num_bytes, void* lds_dst, int voff_bytes) {
+#if __HIP_DEVICE_COMPILE__
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, num_bytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)lds_dst, 4, voff_bytes, 0, 0, 0);
+#endif
+}
+
 // Max / sum of a value with the same value in lane l ^ 32 (v_permlane32_swap).
 __device__ __forceinline__ float pair_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -92,6 +102,35 @@ __device__ __forceinline__ int xcd_swizzle(int id, int total) {
   const int per = total / nx, rem = total % nx;
   const int xcd = id % nx, n = id / nx;
   return xcd * per + (xcd < rem ? xcd : rem) + n;
+}
+
+// Row index with bits 2 and 3 swapped.  Loading the A operand of a 32x32x16 MFMA from
+// row swap_bits23(l % 32) puts, in each lane half h, the 8 consecutive rows 8h..8h+7 of
+// every 16-row group into registers 0..7 and 8..15 of the result -- the k layout of a
+// B operand -- so a transposed product can feed the next MFMA without a shuffle.
+__device__ __forceinline__ int swap_bits23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
+
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+// XOR swizzle of the 16-byte chunks of an unpadded LDS tile row of D bf16 elements:
+// logical chunk c of row r is stored at chunk c ^ swz<D>(r).  For D = 128 (16 chunks)
+// both 16 consecutive rows read at one chunk and 4 consecutive rows read across 4
+// consecutive chunks touch 16 distinct chunk positions (no bank conflicts); for D = 64
+// (8 chunks, two rows per 256-byte bank sweep) rows of equal parity are spread.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) {
+    return 4 * (r & 3) + ((r >> 2) & 3);
+  } else {
+    const int s = (r >> 1) & 7;
+    return s ^ ((s & 1) << 2);
+  }
 }
 
 }  // namespace ra

@@ -299,11 +299,12 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
   const bool f32 = P.elt == 4;  // float32 gradients accumulate straight into the outputs
   const size_t grads = f32 ? 0 : 3 * telems * sizeof(float);
   CallResources R(stream);
-  int rc = R.alloc(recv + nrow * sizeof(float) + grads);
+  int rc = R.alloc(recv + 2 * nrow * sizeof(float) + grads);
   if (rc) return rc;
   char* base = (char*)R.ws;
   float* delta = (float*)(base + recv);
-  float* gq = f32 ? (float*)dq : delta + nrow;
+  float* lse2 = delta + nrow;  // bf16 path: lse in log2 units
+  float* gq = f32 ? (float*)dq : lse2 + nrow;
   float* gk = f32 ? (float*)dk : gq + telems;
   float* gv = f32 ? (float*)dv : gk + telems;
   RA_HIP(launch_zero_f32(gq, (long long)telems, stream));
@@ -312,12 +313,12 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
   if (f32)
     RA_HIP(launch_bwd_pre_f32((const float*)o, (const float*)dO, delta, P.B, P.Sq, P.H, P.D, stream));
   else
-    RA_HIP(launch_bwd_pre_bf16(o, dO, delta, P.B, P.Sq, P.H, P.D, stream));
+    RA_HIP(launch_bwd_pre_bf16(o, dO, lse, delta, lse2, P.B, P.Sq, P.H, P.D, stream));
 
   BwdStep st{};
   st.q = P.q;
   st.dO = dO;
-  st.lse = lse;
+  st.lse = f32 ? lse : lse2;
   st.delta = delta;
   st.dq = gq;
   st.dk = gk;
