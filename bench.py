@@ -79,6 +79,22 @@ def cpu_baseline(B, S, H, D):
     }
 
 
+def recorded_traffic():
+    """HBM bytes per step-kernel launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary, or None if the kernel sources changed since it was taken."""
+    import hashlib
+    prof = os.path.join(ROOT, "profiles", "attn_fwd_S32768_H32_D128_hosts8_traffic.md")
+    srcs = [os.path.join(ROOT, "paper_2310_01889_amd", "csrc", f)
+            for f in ("attn_fwd.hip", "ra_common.h", "ra_kernels.h")]
+    if not os.path.exists(prof):
+        return None
+    h = hashlib.sha256(b"".join(open(f, "rb").read() for f in srcs)).hexdigest()[:16]
+    fields = dict(l.split(": ", 1) for l in open(prof).read().splitlines() if ": " in l and not l.startswith("|"))
+    if fields.get("source_sha256_16", "").strip() != h:
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -138,7 +154,7 @@ def main():
         "tokens_per_s": round(B * S / (ms * 1e-3), 1),
         "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (attention step)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
                      "avg_launch_ms": round(k_avg_ms, 4), "launches": launches},
     }
 
