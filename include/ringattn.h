@@ -112,6 +112,25 @@ int ring_attn_fwd_host(const void* q_blk, const void* k_all, const void* v_all, 
                        int causal, hipStream_t stream);
 
 /*
+ * One host's share of the ring backward (Appendix A backward code seen from host
+ * host_idx), bf16: dq of query block host_idx, and this host's contribution to the float32
+ * dK_j, dV_j that travel with every key/value block j.  Blocks arrive in ring order
+ * (host_idx - t) mod n_hosts; from step 1 on, K_j, V_j and the gradients dK_j, dV_j they carry
+ * are received into the host's double buffer on the side stream, the host adds its
+ * contribution, and the gradients are passed on (copied out) -- three times the bytes of
+ * the forward rotation.
+ *   q_blk, o_blk, dO_blk  in  bf16 [B, c, H, D];  lse_blk in f32 [B, H, c] (ring_attn_fwd_host)
+ *   k_all, v_all          in  bf16 [B, S, H, D]
+ *   dq_blk                out bf16 [B, c, H, D]
+ *   dk_acc, dv_acc        in/out f32 [B, S, H, D]: the gradients the blocks carry when they
+ *                         reach this host; this host's contributions are added.
+ */
+int ring_attn_bwd_host(const void* q_blk, const void* k_all, const void* v_all, const void* o_blk,
+                       const float* lse_blk, const void* dO_blk, void* dq_blk, float* dk_acc,
+                       float* dv_acc, int B, int H, int S, int D, int n_hosts, int host_idx,
+                       int causal, hipStream_t stream);
+
+/*
  * Ring attention forward with an explicit block order, bf16 (checks the permutation
  * invariance that Section 3 relies on: blocks may be folded in any order).
  *   kv_order  HOST pointer, int[n_hosts * n_hosts]; row i is the sequence of key/value

@@ -71,20 +71,20 @@ def attention_rows(q, k, v, rows, causal, scale=None, q_offset=0):
     B, R, H, D = qs.shape
     if scale is None:
         scale = 1.0 / math.sqrt(D)
-    k, v = _as64(k), _as64(v)
     o = np.zeros((B, R, H, v.shape[3]))
     lse = np.zeros((B, H, R))
     for b in range(B):
         for h in range(H):
-            s = (qs[b, :, h, :] @ k[b, :, h, :].T) * scale
+            kh, vh = _as64(k[b, :, h, :]), _as64(v[b, :, h, :])  # one head at a time
+            s = (qs[b, :, h, :] @ kh.T) * scale
             if causal:
                 qpos = (q_offset + rows)[:, None]
-                kpos = np.arange(k.shape[1])[None, :]
+                kpos = np.arange(kh.shape[0])[None, :]
                 s = np.where(kpos > qpos, -np.inf, s)
             m = s.max(axis=1)
             p = np.exp(s - m[:, None])
             den = p.sum(axis=1)
-            o[b, :, h, :] = (p @ v[b, :, h, :]) / den[:, None]
+            o[b, :, h, :] = (p @ vh) / den[:, None]
             lse[b, h, :] = m + np.log(den)
     return o, lse
 
@@ -119,3 +119,29 @@ def attention_bwd(q, k, v, do, causal, scale=None, q_offset=0, row_chunk=1024):
                 dk[b, :, h, :] += (ds.T @ qh) * scale
                 dv[b, :, h, :] += phat.T @ doh
     return dq, dk, dv
+
+
+def attention_bwd_rows(q, k, v, do, rows, causal, scale=None, q_offset=0):
+    """Rows ``rows`` of dq only (row r of dq depends on query row r, its upstream gradient
+    and every key/value).  Same definition as attention_bwd restricted to those rows;
+    k and v are upcast one head at a time.  Returns dq_rows [B, len(rows), H, D]."""
+    rows = np.asarray(rows, dtype=np.int64)
+    qs, dos = _as64(q)[:, rows], _as64(do)[:, rows]
+    B, R, H, D = qs.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    dq = np.zeros((B, R, H, D))
+    for b in range(B):
+        for h in range(H):
+            kh, vh = _as64(k[b, :, h, :]), _as64(v[b, :, h, :])
+            s = (qs[b, :, h, :] @ kh.T) * scale
+            if causal:
+                qpos = (q_offset + rows)[:, None]
+                s = np.where(np.arange(kh.shape[0])[None, :] > qpos, -np.inf, s)
+            p = np.exp(s - s.max(axis=1)[:, None])
+            phat = p / p.sum(axis=1)[:, None]
+            oh = phat @ vh
+            delta = (dos[b, :, h, :] * oh).sum(axis=1)
+            ds = phat * (dos[b, :, h, :] @ vh.T - delta[:, None])
+            dq[b, :, h, :] = (ds @ kh) * scale
+    return dq

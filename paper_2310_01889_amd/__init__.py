@@ -18,7 +18,7 @@ import torch
 __all__ = [
     "RingAttnError", "library_path", "load", "exported_symbols",
     "ring_attn_fwd", "ring_attn_bwd", "ring_attn_fwd_f32", "ring_attn_bwd_f32",
-    "ring_attn_fwd_host", "ring_attn_fwd_ordered", "blockwise_ffn", "blockwise_ffn_bwd",
+    "ring_attn_fwd_host", "ring_attn_bwd_host", "ring_attn_fwd_ordered", "blockwise_ffn", "blockwise_ffn_bwd",
     "blockwise_linear", "blockwise_linear_bwd", "ring_layer_fwd", "ring_layer_bwd",
     "attention_fwd", "attention_bwd",
     "ACT_GELU_ERF", "ACT_RELU", "ACT_GELU_TANH",
@@ -36,6 +36,7 @@ _SIGS = {
     "ring_attn_bwd": [_P] * 9 + [_I] * 6 + [_P],
     "ring_attn_bwd_f32": [_P] * 9 + [_I] * 6 + [_P],
     "ring_attn_fwd_host": [_P] * 5 + [_I] * 7 + [_P],
+    "ring_attn_bwd_host": [_P] * 9 + [_I] * 7 + [_P],
     "ring_attn_fwd_ordered": [_P] * 5 + [_I] * 6 + [_P, _P],
     "blockwise_ffn": [_P] * 6 + [_I] * 5 + [_P],
     "blockwise_ffn_bwd": [_P] * 10 + [_I] * 5 + [_P],
@@ -178,6 +179,17 @@ def ring_attn_fwd_host(q_blk, k_all, v_all, o_blk, lse_blk, n_hosts, host_idx, c
     _call("ring_attn_fwd_host", _ptr(q_blk, bf, "q_blk"), _ptr(k_all, bf, "k_all"), _ptr(v_all, bf, "v_all"),
           _ptr(o_blk, bf, "o_blk"), _ptr(lse_blk, torch.float32, "lse_blk"), B, H, S, D, int(n_hosts),
           int(host_idx), int(causal), _stream(stream))
+
+
+def ring_attn_bwd_host(q_blk, k_all, v_all, o_blk, lse_blk, dO_blk, dq_blk, dk_acc, dv_acc, n_hosts, host_idx, causal,
+                       stream=None):
+    B, c, H, D = _bshd(q_blk)
+    S = int(k_all.shape[1])
+    bf, f = torch.bfloat16, torch.float32
+    _call("ring_attn_bwd_host", _ptr(q_blk, bf, "q_blk"), _ptr(k_all, bf, "k_all"), _ptr(v_all, bf, "v_all"),
+          _ptr(o_blk, bf, "o_blk"), _ptr(lse_blk, f, "lse_blk"), _ptr(dO_blk, bf, "dO_blk"), _ptr(dq_blk, bf, "dq_blk"),
+          _ptr(dk_acc, f, "dk_acc"), _ptr(dv_acc, f, "dv_acc"), B, H, S, D, int(n_hosts), int(host_idx), int(causal),
+          _stream(stream))
 
 
 def ring_attn_fwd_ordered(q, k, v, o, lse, n_hosts, causal, kv_order, stream=None):

@@ -353,6 +353,134 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
 }
 
 // ---------------------------------------------------------------------------------
+// Backward, one host's share: the key/value blocks arrive in ring order together with the
+// float32 dK/dV they carry; this host adds its contribution and passes them on.
+// ---------------------------------------------------------------------------------
+static int copy_rows(void* dst, size_t dpitch, const void* src, size_t spitch, size_t width, int height,
+                     hipStream_t st) {
+  if (height == 1 || (dpitch == width && spitch == width)) {
+    RA_HIP(hipMemcpyAsync(dst, src, width * height, hipMemcpyDeviceToDevice, st));
+  } else {
+    RA_HIP(hipMemcpy2DAsync(dst, dpitch, src, spitch, width, height, hipMemcpyDeviceToDevice, st));
+  }
+  return RA_OK;
+}
+
+static int run_bwd_host(const void* q_blk, const void* k_all, const void* v_all, const void* o_blk,
+                        const float* lse_blk, const void* dO_blk, void* dq_blk, float* dk_acc, float* dv_acc,
+                        int B, int H, int S, int D, int N, int host, int causal, hipStream_t stream) {
+  const int c = S / N;
+  const size_t rowe = (size_t)H * D;           // elements per token row
+  const size_t blk = (size_t)c * rowe;         // elements of one block (per batch)
+  const size_t nrow = (size_t)B * H * c;
+  const size_t qel = (size_t)B * blk;
+  // workspace: K/V slots (bf16) and dK/dV slots (float32), 2 each; Delta, lse2; dq (float32)
+  const size_t kv_slot = qel * 2, g_slot = qel * 4;
+  CallResources R(stream);
+  int rc = R.alloc(4 * kv_slot + 4 * g_slot + 2 * nrow * 4 + qel * 4);
+  if (rc) return rc;
+  char* base = (char*)R.ws;
+  auto kslot = [&](int s) { return base + s * kv_slot; };
+  auto vslot = [&](int s) { return base + (2 + s) * kv_slot; };
+  auto dkslot = [&](int s) { return (float*)(base + 4 * kv_slot + s * g_slot); };
+  auto dvslot = [&](int s) { return (float*)(base + 4 * kv_slot + (2 + s) * g_slot); };
+  float* delta = (float*)(base + 4 * kv_slot + 4 * g_slot);
+  float* lse2 = delta + nrow;
+  float* dq32 = lse2 + nrow;
+  RA_HIP(launch_zero_f32(dq32, (long long)qel, stream));
+  RA_HIP(launch_bwd_pre_bf16(o_blk, dO_blk, lse_blk, delta, lse2, B, c, H, D, stream));
+
+  auto blk_of = [&](int t) { return ((host - t) % N + N) % N; };
+  auto active = [&](int t) { return !causal || blk_of(t) <= host; };
+  hipStream_t side = stream;
+  rc = side_stream(&side);
+  if (rc) return rc;
+  hipEvent_t ev;
+  if ((rc = R.event(&ev))) return rc;
+  RA_HIP(hipEventRecord(ev, stream));
+  RA_HIP(hipStreamWaitEvent(side, ev, 0));
+  std::vector<hipEvent_t> ev_recv(N + 2, nullptr);
+  // receive block blk_of(t) with its carried gradients into slot t & 1
+  auto receive = [&](int t) -> int {
+    if (t >= N || !active(t)) return RA_OK;
+    const int j = blk_of(t), s2 = t & 1;
+    const size_t off = (size_t)j * blk;
+    int r = copy_rows(kslot(s2), blk * 2, (const char*)k_all + off * 2, (size_t)S * rowe * 2, blk * 2, B, side);
+    if (!r) r = copy_rows(vslot(s2), blk * 2, (const char*)v_all + off * 2, (size_t)S * rowe * 2, blk * 2, B, side);
+    if (!r) r = copy_rows(dkslot(s2), blk * 4, dk_acc + off, (size_t)S * rowe * 4, blk * 4, B, side);
+    if (!r) r = copy_rows(dvslot(s2), blk * 4, dv_acc + off, (size_t)S * rowe * 4, blk * 4, B, side);
+    if (r) return r;
+    if ((r = R.event(&ev_recv[t]))) return r;
+    RA_HIP(hipEventRecord(ev_recv[t], side));
+    return RA_OK;
+  };
+  // pass block blk_of(t) on: its carried gradients leave slot t & 1
+  auto send = [&](int t) -> int {
+    const int j = blk_of(t), s2 = t & 1;
+    const size_t off = (size_t)j * blk;
+    int r = copy_rows(dk_acc + off, (size_t)S * rowe * 4, dkslot(s2), blk * 4, blk * 4, B, side);
+    if (!r) r = copy_rows(dv_acc + off, (size_t)S * rowe * 4, dvslot(s2), blk * 4, blk * 4, B, side);
+    return r;
+  };
+  if ((rc = receive(1)) || (rc = receive(2))) return rc;
+
+  BwdStep st{};
+  st.q = q_blk;
+  st.dO = dO_blk;
+  st.lse = lse2;
+  st.delta = delta;
+  st.dq = dq32;
+  st.q_bstride = (long long)blk;
+  st.B = B;
+  st.H = H;
+  st.Sq = c;
+  st.c = c;
+  st.causal = causal;
+  st.scale = 1.0f / sqrtf((float)D);
+  st.n_slots = 1;
+  for (int t = 0; t < N; ++t) {
+    if (!active(t)) continue;
+    const int j = blk_of(t);
+    StepHost& h = st.host[0];
+    h = StepHost{};
+    if (t == 0) {  // the host's own block and the gradients it carries: in place
+      h.k = (const char*)k_all + (size_t)j * blk * 2;
+      h.v = (const char*)v_all + (size_t)j * blk * 2;
+      h.kv_bstride = (long long)S * rowe;
+      st.dk = dk_acc + (size_t)j * blk;
+      st.dv = dv_acc + (size_t)j * blk;
+      st.dkv_bstride = (long long)S * rowe;
+    } else {
+      RA_HIP(hipStreamWaitEvent(stream, ev_recv[t], 0));
+      h.k = kslot(t & 1);
+      h.v = vslot(t & 1);
+      h.kv_bstride = (long long)blk;
+      st.dk = dkslot(t & 1);
+      st.dv = dvslot(t & 1);
+      st.dkv_bstride = (long long)blk;
+    }
+    h.q_row0 = 0;
+    h.q_pos0 = host * c;
+    h.k_pos0 = j * c;
+    st.dkv_row0[0] = 0;
+    RA_HIP(timed_launch(RA_KERNEL_ATTN_BWD, stream, [&] { return launch_bwd_bf16(st, D, stream); }));
+    if (t >= 1) {
+      hipEvent_t done;
+      if ((rc = R.event(&done))) return rc;
+      RA_HIP(hipEventRecord(done, stream));
+      RA_HIP(hipStreamWaitEvent(side, done, 0));
+      if ((rc = send(t)) || (rc = receive(t + 2))) return rc;
+    }
+  }
+  hipEvent_t tail;
+  if ((rc = R.event(&tail))) return rc;
+  RA_HIP(hipEventRecord(tail, side));
+  RA_HIP(hipStreamWaitEvent(stream, tail, 0));
+  RA_HIP(launch_cast_f32_bf16(dq32, dq_blk, (long long)qel, stream));
+  return RA_OK;
+}
+
+// ---------------------------------------------------------------------------------
 // Argument validation
 // ---------------------------------------------------------------------------------
 static int validate(int B, int H, int S, int D, int N, int causal, int tile) {
@@ -463,6 +591,20 @@ int ring_attn_fwd_ordered(const void* q, const void* k, const void* v, void* o, 
     }
   }
   return run_fwd(P, o, lse, stream);
+}
+
+int ring_attn_bwd_host(const void* q_blk, const void* k_all, const void* v_all, const void* o_blk,
+                       const float* lse_blk, const void* dO_blk, void* dq_blk, float* dk_acc, float* dv_acc, int B,
+                       int H, int S, int D, int n_hosts, int host_idx, int causal, hipStream_t stream) {
+  g_err.clear();
+  if (!q_blk || !k_all || !v_all || !o_blk || !lse_blk || !dO_blk || !dq_blk || !dk_acc || !dv_acc)
+    return set_err(RA_EINVAL, "null pointer argument");
+  int rc = validate(B, H, S, D, n_hosts, causal, 128);
+  if (rc) return rc;
+  if (host_idx < 0 || host_idx >= n_hosts)
+    return set_err(RA_EINVAL, "host_idx=%d outside [0, n_hosts=%d)", host_idx, n_hosts);
+  return run_bwd_host(q_blk, k_all, v_all, o_blk, lse_blk, dO_blk, dq_blk, dk_acc, dv_acc, B, H, S, D, n_hosts,
+                      host_idx, causal, stream);
 }
 
 int ring_attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse, const void* dO,

@@ -136,3 +136,15 @@ def test_gradient_invariants(causal):
     dq, dk, dv = A.attention_bwd(q, k, v, do, causal)
     np.testing.assert_allclose(dk.sum(axis=1), 0.0, atol=1e-12)
     np.testing.assert_allclose(dv.sum(axis=1), do.sum(axis=1), atol=1e-12)
+
+
+def test_gradient_rows_match_full_backward():
+    q, k, v, do = (_rand(s, 2, 40, 2, 8) for s in (33, 34, 35, 36))
+    dq, _, _ = A.attention_bwd(q, k, v, do, True)
+    rows = np.array([0, 3, 17, 39])
+    np.testing.assert_allclose(A.attention_bwd_rows(q, k, v, do, rows, True), dq[:, rows], atol=1e-13)
+    # a later query block against all keys (global positions)
+    dqb, dkb, dvb = A.attention_bwd(q[:, 24:], k, v, do[:, 24:], True, q_offset=24)
+    np.testing.assert_allclose(dqb, dq[:, 24:], atol=1e-13)
+    np.testing.assert_allclose(A.attention_bwd_rows(q[:, 24:], k, v, do[:, 24:], [0, 15], True, q_offset=24),
+                               dq[:, [24, 39]], atol=1e-13)
