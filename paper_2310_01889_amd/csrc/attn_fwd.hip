@@ -50,10 +50,24 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   constexpr int NDT = D / 32;  // 32-row output tiles of O^T
   constexpr int CPR = D / 8;   // 16-byte chunks per row
   constexpr int ROWS_PER_LOAD = 64 / CPR;               // rows filled by one 1 KB wave load
-  constexpr int LOADS = kBN / 4 / ROWS_PER_LOAD;        // loads per wave per tile (16 rows/wave)
+  constexpr int RPW = kBN / 4;                           // tile rows each wave fills
+  constexpr int LOADS = RPW / ROWS_PER_LOAD;             // 1 KB loads per wave per tile
   constexpr int TILE = kBN * D;                          // elements per tile
-  __shared__ __attribute__((aligned(1024))) bf16 sK[2][TILE];
-  __shared__ __attribute__((aligned(1024))) bf16 sV[2][TILE];
+  // Four separate LDS objects (not one [2][TILE] array per operand): the compiler then
+  // knows that reads of one buffer do not alias direct-to-LDS loads in flight into the
+  // other, and does not wait for those loads before every read.
+  __shared__ __attribute__((aligned(1024))) bf16 sK0[TILE];
+  __shared__ __attribute__((aligned(1024))) bf16 sK1[TILE];
+  __shared__ __attribute__((aligned(1024))) bf16 sV0[TILE];
+  __shared__ __attribute__((aligned(1024))) bf16 sV1[TILE];
+  auto kbuf = [&](auto Bc) __attribute__((always_inline)) -> bf16* {
+    if constexpr (decltype(Bc)::value == 0) return sK0; else return sK1;
+  };
+  auto vbuf = [&](auto Bc) __attribute__((always_inline)) -> bf16* {
+    if constexpr (decltype(Bc)::value == 0) return sV0; else return sV1;
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
 
   const int n_qt = p.c / kBM;
   const int BH = p.B * p.H;
@@ -112,20 +126,36 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   }
 
   // ---- Q in registers: B operand of S^T = K Q^T (n = query, k = dim) ---------------
+  // Q is stored pre-multiplied by log2(e)/sqrt(D) (rounded to bf16), so the products
+  // come out as scaled scores in log2 units.
+  const float sl2 = p.scale * kLog2e;
   bf16x8 qreg[NKK];
   {
     const bf16* qrow = qbase + (long long)qr * rs;
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) qreg[kk] = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
+    for (int kk = 0; kk < NKK; ++kk) {
+      const bf16x8 t = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qreg[kk][e] = (bf16)((float)t[e] * sl2);
+    }
   }
+  // The score accumulators start from -m_eff (m_eff = running maximum, 0 while it is
+  // still -inf), so each MFMA chain yields s - m_eff directly.  thr: a row whose new
+  // scores exceed it forces a rescale (kTau above the maximum, any visible key at all
+  // while the maximum is still -inf).
+  float m_eff = (m_run == -INFINITY) ? 0.f : m_run;
+  float thr = (m_run == -INFINITY) ? -INFINITY : kTau;
+  f32x16 minit;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) minit[i] = -m_eff;
 
   // ---- direct-to-LDS staging: each wave fills 16 rows of a tile ---------------------
-  // load j of a wave covers rows wave*16 + j*ROWS_PER_LOAD + lane / CPR; the lane's
+  // load j of a wave covers rows wave*RPW + j*ROWS_PER_LOAD + lane / CPR; the lane's
   // physical chunk is lane % CPR, its logical (global) chunk that ^ swz(row).
   int goff[LOADS];  // byte offsets from the tile base
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
-    const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
+    const int r = wave * RPW + j * ROWS_PER_LOAD + lane / CPR;
     goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
   }
   // buffer loads with the LDS flag: the tile base is a wave-uniform descriptor, so the
@@ -133,10 +163,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   auto dload = [&](const bf16* src_tile, bf16* dst_tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j)
-      buffer_load_lds16(src_tile, kBN * rs * 2, dst_tile + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16(src_tile, kBN * rs * 2, dst_tile + (wave * RPW + j * ROWS_PER_LOAD) * D, goff[j]);
   };
-  auto load_k = [&](int it, int buf) __attribute__((always_inline)) { dload(kbase + (long long)it * kBN * rs, sK[buf]); };
-  auto load_v = [&](int it, int buf) __attribute__((always_inline)) { dload(vbase + (long long)it * kBN * rs, sV[buf]); };
+  auto load_k = [&](int it, auto Bc) __attribute__((always_inline)) { dload(kbase + (long long)it * kBN * rs, kbuf(Bc)); };
+  auto load_v = [&](int it, auto Bc) __attribute__((always_inline)) { dload(vbase + (long long)it * kBN * rs, vbuf(Bc)); };
 
   // ---- per-lane LDS read offsets (elements), fixed across tiles ----------------------
   // row reads of K: row 32 mt + swap_bits23(l32), logical chunk 2 kk + hi
@@ -156,15 +186,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       voff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
 
-  const float sl2 = p.scale * kLog2e;
   // S^T = K Q^T for the 64 keys of K buffer `buf` x this wave's 32 queries
   auto scores = [&](const bf16* kt, f32x16* sacc) __attribute__((always_inline)) {
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
+      sacc[mt] = mfma32(*(const bf16x8*)(kt + 32 * mt * D + koff[0]), qreg[0], minit);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[mt][i] = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
+      for (int kk = 1; kk < NKK; ++kk)
         sacc[mt] = mfma32(*(const bf16x8*)(kt + 32 * mt * D + koff[kk]), qreg[kk], sacc[mt]);
     }
   };
@@ -176,40 +204,42 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   // the matrix cores, the exponentials of tile it on the vector ALUs and O += V P for
   // tile it, interleaved (sched_group_barrier); the running-max decision for tile it+1
   // closes the region, so the only branch (the rare rescale) sits between tiles.
-  auto decide_max = [&](float mx) __attribute__((always_inline)) {
-    const float mx2 = pair_max(mx) * sl2;
-    if (__builtin_amdgcn_ballot_w64(mx2 > m_run + kTau)) {
-      const float m_new = fmaxf(m_run, mx2);
+  // Lazy rescale (online softmax, log2 domain).  Each lane owns one query; the partner
+  // lane l^32 holds the other half of its keys.  The running maximum is raised only
+  // when a row's new scores exceed it by more than kTau, so probabilities stay below
+  // 2^kTau and the rescale of the accumulator -- a wave-uniform branch -- is rare.
+  // mx: this lane's maximum of the tile's s - m_eff; sc: the tile's scores, shifted here
+  // to the new maximum.
+  auto rescale = [&](float mx, f32x16* sc) __attribute__((always_inline)) {
+    const float mx2 = pair_max(mx);
+    if (__builtin_amdgcn_ballot_w64(mx2 > thr)) {
+      const float m_new = fmaxf(m_run, m_eff + mx2);
+      const float m_new_eff = (m_new == -INFINITY) ? 0.f : m_new;
       const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+      const float delta = m_new_eff - m_eff;
       l_run *= alpha;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sc[mt][i] -= delta;
       m_run = m_new;
+      m_eff = m_new_eff;
+      thr = (m_new == -INFINITY) ? -INFINITY : kTau;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) minit[i] = -m_eff;
     }
   };
   auto decide = [&](f32x16* sc) __attribute__((always_inline)) {
-    // online softmax, log2 domain; each lane owns one query and the partner lane l^32
-    // holds the other half of its keys.  The running maximum is raised only when a
-    // row's new maximum exceeds it by more than kTau (probabilities then stay below
-    // 2^kTau), so the rescale of the accumulator -- a wave-uniform branch -- is rare.
     float mx = -INFINITY;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[mt][i]);
-    const float mx2 = pair_max(mx) * sl2;
-    if (__builtin_amdgcn_ballot_w64(mx2 > m_run + kTau)) {
-      const float m_new = fmaxf(m_run, mx2);
-      const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
-      m_run = m_new;
-    }
+    rescale(mx, sc);
   };
   auto mask = [&](f32x16* sc, int it) __attribute__((always_inline)) {
     const int kpos0 = hs.k_pos0 + it * kBN;
@@ -223,17 +253,16 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   };
   // P = exp2(s log2e/sqrt(D) - m) in bf16 and O^T += V^T P^T for one tile
   auto softmax_pv = [&](const f32x16* sc, const bf16* vt) __attribute__((always_inline)) {
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float rsum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       u32x4 w;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float p0 = fast_exp2(fmaf(sc[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
-        const float p1 = fast_exp2(fmaf(sc[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
-        rsum += p0 + p1;
+        const float p0 = fast_exp2(sc[kb >> 1][8 * (kb & 1) + 2 * j]);
+        const float p1 = fast_exp2(sc[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
         w[j] = pack_bf16x2(p0, p1);
+        rsum = dot2_bf16_ones(w[j], rsum);  // row sum of the bf16 probabilities used
       }
       const bf16x8 pb = __builtin_bit_cast(bf16x8, w);
 #pragma unroll
@@ -248,18 +277,20 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   };
 
   if (nt > 0) {
-    load_k(0, 0);
-    load_v(0, 0);
-    if (nt > 1) load_k(1, 1);
+    load_k(0, I0{});
+    load_v(0, I0{});
+    if (nt > 1) load_k(1, I1{});
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   f32x16 s_cur[2];
   if (nt > 0) {
-    scores(sK[0], s_cur);
+    scores(sK0, s_cur);
     if (n_full == 0) mask(s_cur, 0);
     decide(s_cur);
   }
+  // the first loop step reloads the buffer of K tile 0: every wave must have read it
+  if (nt > 2) __syncthreads();
 
   // tile it with a successor; B = it & 1 at compile time, MN: tile it+1 needs the mask.
   // The region is laid out by hand in 20 steps separated by scheduling fences: step s
@@ -271,11 +302,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     constexpr int B = decltype(Bc)::value;
     constexpr bool MN = decltype(Mc)::value;
     static_assert(NKK == 8 && NDT == 4, "hand schedule written for D = 128");
-    if (it + 2 < nt) load_k(it + 2, B);
-    load_v(it + 1, B ^ 1);
-    const bf16* kt = sK[B ^ 1];
-    const bf16* vt = sV[B];
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    if (it + 2 < nt) load_k(it + 2, Bc);
+    load_v(it + 1, std::integral_constant<int, B ^ 1>{});
+    const bf16* kt = kbuf(std::integral_constant<int, B ^ 1>{});
+    const bf16* vt = vbuf(Bc);
     f32x16 s_next[2];
     bf16x8 kop[16], vop[16], pb[4];
     uint32_t w[4][4];
@@ -298,8 +328,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       if constexpr (S + kPF >= 4 && S + kPF < 20) read_v(std::integral_constant<int, S + kPF - 4>{});
       if constexpr (S < 16) {
         constexpr int mt = S / NKK, kk = S % NKK;
-        if constexpr (kk == 0) s_next[mt] = f32x16{};
-        s_next[mt] = mfma32(kop[S], qreg[kk], s_next[mt]);
+        s_next[mt] = mfma32(kop[S], qreg[kk], kk == 0 ? minit : s_next[mt]);
       }
       if constexpr (S >= 4) {
         constexpr int q = S - 4, kb = q / NDT, dt = q % NDT;
@@ -308,8 +337,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       }
       if constexpr (S < 16) {
         constexpr int kb = S / 4, j = S % 4;
-        const float p0 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j], sl2, -m_use));
-        const float p1 = fast_exp2(fmaf(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1], sl2, -m_use));
+        const float p0 = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j]);
+        const float p1 = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
         w[kb][j] = pack_bf16x2(p0, p1);
         rs2[j] = dot2_bf16_ones(w[kb][j], rs2[j]);  // row sum of the bf16 probabilities used
       } else if constexpr (S < 18) {
@@ -323,7 +352,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       __builtin_amdgcn_sched_barrier(0);
     });
     l_run += (rs2[0] + rs2[1]) + (rs2[2] + rs2[3]);
-    decide_max(fmaxf(mxa, mxb));
+    rescale(fmaxf(mxa, mxb), s_next);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tiles it+1 (V) and it+2 (K) landed
     __syncthreads();
     s_cur[0] = s_next[0];
@@ -333,11 +362,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   auto body_plain = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
     constexpr int B = decltype(Bc)::value;
     constexpr bool MN = decltype(Mc)::value;
-    if (it + 2 < nt) load_k(it + 2, B);
-    load_v(it + 1, B ^ 1);
+    if (it + 2 < nt) load_k(it + 2, Bc);
+    load_v(it + 1, std::integral_constant<int, B ^ 1>{});
     f32x16 s_next[2];
-    scores(sK[B ^ 1], s_next);
-    softmax_pv(s_cur, sV[B]);
+    scores(kbuf(std::integral_constant<int, B ^ 1>{}), s_next);
+    softmax_pv(s_cur, vbuf(Bc));
     if (MN) mask(s_next, it + 1);
     decide(s_next);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -367,9 +396,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     run(std::true_type{}, split, nt - 1);
     // last tile: no successor
     if ((nt - 1) & 1)
-      softmax_pv(s_cur, sV[1]);
+      softmax_pv(s_cur, sV1);
     else
-      softmax_pv(s_cur, sV[0]);
+      softmax_pv(s_cur, sV0);
   }
 
   // ---- end of step: finalise or save the running state -------------------------------
