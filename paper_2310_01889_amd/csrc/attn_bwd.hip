@@ -86,10 +86,19 @@ template <int D>
 __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) {
   constexpr int NKK = D / 16, NDT = D / 32, CPR = D / 8;
   constexpr int ROWS_PER_LOAD = 64 / CPR, LOADS = kQB / 4 / ROWS_PER_LOAD;
-  __shared__ __attribute__((aligned(1024))) bf16 sQ[2][kQB * D];
-  __shared__ __attribute__((aligned(1024))) bf16 sO[2][kQB * D];  // dO tile
-  __shared__ __attribute__((aligned(256))) float sL[2][kQB];       // lse * log2e
-  __shared__ __attribute__((aligned(256))) float sD[2][kQB];       // Delta
+  // one LDS object per buffer, so that reads of one buffer are known not to alias the
+  // direct-to-LDS loads in flight into the other (else the compiler waits for them)
+  __shared__ __attribute__((aligned(1024))) bf16 sQ0[kQB * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sQ1[kQB * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sO0[kQB * D];  // dO tile
+  __shared__ __attribute__((aligned(1024))) bf16 sO1[kQB * D];
+  __shared__ __attribute__((aligned(256))) float sL0[kQB];       // lse * log2e
+  __shared__ __attribute__((aligned(256))) float sL1[kQB];
+  __shared__ __attribute__((aligned(256))) float sD0[kQB];       // Delta
+  __shared__ __attribute__((aligned(256))) float sD1[kQB];
+  auto pick = [](auto Bc, auto* a, auto* b) __attribute__((always_inline)) {
+    if constexpr (decltype(Bc)::value == 0) return a; else return b;
+  };
 
   const int n_kt = p.c / kKB;
   const int BH = p.B * p.H;
@@ -140,15 +149,15 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
     goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
   }
-  auto load_tile = [&](int qt, int buf) __attribute__((always_inline)) {
+  auto load_tile = [&](int qt, auto Bc) __attribute__((always_inline)) {
     const long long t0 = (long long)(hs.q_row0 + qt * kQB) * rs;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      buffer_load_lds16(qbase + t0, kQB * rs * 2, &sQ[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
-      buffer_load_lds16(obase + t0, kQB * rs * 2, &sO[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
+      buffer_load_lds16(qbase + t0, kQB * rs * 2, pick(Bc, sQ0, sQ1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16(obase + t0, kQB * rs * 2, pick(Bc, sO0, sO1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
     }
-    if (wave == 0) buffer_load_lds4(p.lse + lrow0 + qt * kQB, kQB * 4, sL[buf], 4 * lane);
-    if (wave == 1) buffer_load_lds4(p.delta + lrow0 + qt * kQB, kQB * 4, sD[buf], 4 * lane);
+    if (wave == 0) buffer_load_lds4(p.lse + lrow0 + qt * kQB, kQB * 4, pick(Bc, sL0, sL1), 4 * lane);
+    if (wave == 1) buffer_load_lds4(p.delta + lrow0 + qt * kQB, kQB * 4, pick(Bc, sD0, sD1), 4 * lane);
   };
   const int qrow = swap_bits23(l32);
   int roff[NKK];
@@ -169,9 +178,11 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   auto body = [&](auto Bc, auto Mc, int qt) __attribute__((always_inline)) {
     constexpr int B = decltype(Bc)::value;
     constexpr bool MASK = decltype(Mc)::value;
-    if (qt + 1 < n_qtiles) load_tile(qt + 1, B ^ 1);
-    const bf16* qtl = sQ[B];
-    const bf16* otl = sO[B];
+    if (qt + 1 < n_qtiles) load_tile(qt + 1, std::integral_constant<int, B ^ 1>{});
+    const bf16* qtl = pick(Bc, sQ0, sQ1);
+    const bf16* otl = pick(Bc, sO0, sO1);
+    const float* sDb = pick(Bc, sD0, sD1);
+    const float* sLb = pick(Bc, sL0, sL1);
     const int qpos0 = hs.q_pos0 + qt * kQB;
     // S and dP (rows = queries 32 qm + 16 (i/8) + 8 hi + i%8 of the tile)
     f32x16 sacc[2], dpacc[2];
@@ -180,8 +191,8 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
 #pragma unroll
       for (int hb = 0; hb < 2; ++hb) {
         const int q0 = 32 * qm + 16 * hb + 8 * hi;
-        const f32x4 da = *(const f32x4*)&sD[B][q0];
-        const f32x4 db = *(const f32x4*)&sD[B][q0 + 4];
+        const f32x4 da = *(const f32x4*)&sDb[q0];
+        const f32x4 db = *(const f32x4*)&sDb[q0 + 4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           dpacc[qm][8 * hb + e] = -da[e];
@@ -201,8 +212,8 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     for (int kb = 0; kb < 4; ++kb) {
       const int qm = kb >> 1, hb = kb & 1;
       const int q0 = 32 * qm + 16 * hb + 8 * hi;
-      const f32x4 la = *(const f32x4*)&sL[B][q0];
-      const f32x4 lb = *(const f32x4*)&sL[B][q0 + 4];
+      const f32x4 la = *(const f32x4*)&sLb[q0];
+      const f32x4 lb = *(const f32x4*)&sLb[q0 + 4];
       u32x4 wp, ws;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -243,7 +254,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     }
     if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
   };
-  if (qt0 < n_qtiles) load_tile(qt0, 0);
+  if (qt0 < n_qtiles) load_tile(qt0, std::integral_constant<int, 0>{});
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   run(std::true_type{}, qt0, qt_free);
@@ -286,8 +297,14 @@ template <int D>
 __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   constexpr int NKK = D / 16, NDT = D / 32, CPR = D / 8;
   constexpr int ROWS_PER_LOAD = 64 / CPR, LOADS = kKK / 4 / ROWS_PER_LOAD;
-  __shared__ __attribute__((aligned(1024))) bf16 sK[2][kKK * D];
-  __shared__ __attribute__((aligned(1024))) bf16 sV[2][kKK * D];
+  // one LDS object per buffer (see the dK/dV kernel)
+  __shared__ __attribute__((aligned(1024))) bf16 sK0[kKK * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sK1[kKK * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV0[kKK * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sV1[kKK * D];
+  auto pick = [](auto Bc, auto* a, auto* b) __attribute__((always_inline)) {
+    if constexpr (decltype(Bc)::value == 0) return a; else return b;
+  };
 
   const int n_qt = p.c / kQQ;
   const int BH = p.B * p.H;
@@ -316,6 +333,11 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
       qreg[kk] = *(const bf16x8*)((const bf16*)p.q + off + 16 * kk);
       oreg[kk] = *(const bf16x8*)((const bf16*)p.dO + off + 16 * kk);
     }
+    // consume the loads here: otherwise the compiler, unsure whether they are still in
+    // flight, waits on the load counter inside the loop, where it also counts the
+    // prefetch of the next tile
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) asm volatile("" ::"v"(qreg[kk]), "v"(oreg[kk]));
   }
   f32x16 dqacc[NDT];
 #pragma unroll
@@ -339,12 +361,12 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
     const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
     goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
   }
-  auto load_tile = [&](int it, int buf) __attribute__((always_inline)) {
+  auto load_tile = [&](int it, auto Bc) __attribute__((always_inline)) {
     const long long t0 = (long long)it * kKK * rs;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      buffer_load_lds16(kbase + t0, kKK * rs * 2, &sK[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
-      buffer_load_lds16(vbase + t0, kKK * rs * 2, &sV[buf][(wave * 16 + j * ROWS_PER_LOAD) * D], goff[j]);
+      buffer_load_lds16(kbase + t0, kKK * rs * 2, pick(Bc, sK0, sK1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16(vbase + t0, kKK * rs * 2, pick(Bc, sV0, sV1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
     }
   };
   // row reads (A operand, rows 32 mt + swap_bits23(l32)) and transpose reads of the tiles
@@ -367,9 +389,9 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
     constexpr int B = decltype(Bc)::value;
     constexpr bool MASK = decltype(Mc)::value;
-    if (it + 1 < nt) load_tile(it + 1, B ^ 1);
-    const bf16* kt = sK[B];
-    const bf16* vt = sV[B];
+    if (it + 1 < nt) load_tile(it + 1, std::integral_constant<int, B ^ 1>{});
+    const bf16* kt = pick(Bc, sK0, sK1);
+    const bf16* vt = pick(Bc, sV0, sV1);
     f32x16 sacc[2], dpacc[2];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
@@ -426,7 +448,7 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
     }
     if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
   };
-  if (nt > 0) load_tile(0, 0);
+  if (nt > 0) load_tile(0, std::integral_constant<int, 0>{});
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   run(std::false_type{}, 0, n_full);
