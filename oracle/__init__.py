@@ -19,6 +19,10 @@ Modules
                 activations used here (GeLU-erf, ReLU, GeLU-tanh), its blockwise
                 form (Section 2, "Blockwise Parallel Transformers"), and the
                 projection ``y = x w (+ residual)``; forward and backward.
+  decode     -- ring decode (the paper's appendix on inference): a few query tokens
+                at the end of a long key/value cache that is split in host blocks; the
+                blocks circulate past the queries in ring order and are folded into
+                their running softmax state.
   layer      -- one transformer layer as Algorithm 1 composes it: projections,
                 ring attention, output projection with residual, blockwise FFN with
                 residual; forward and backward.
@@ -26,7 +30,7 @@ Modules
 Every function takes and returns float64 arrays.  Inputs in bf16 are passed in already
 rounded (the exact values the GPU sees), then upcast.
 
-Parity status: attention forward/backward, ring bookkeeping and FFN are pinned by the
+Parity status: attention forward/backward, ring bookkeeping, ring decode and FFN are pinned by the
 tests in tests/test_oracle_*.py (closed forms, invariants, brute force, finite
 differences, library routines).  The layer composition is pinned only to the
 composition defined in ``layer`` (the paper does not fix norms, biases or the

@@ -80,3 +80,29 @@ def test_transposed_weight_gradient_is_caught(monkeypatch):
     orig = F.linear_bwd
     monkeypatch.setattr(F, "linear_bwd", lambda x, w, dy: (orig(x, w, dy)[0], (np.asarray(dy).T @ np.asarray(x)).T[::-1]))
     _fails(TF.test_linear_forward_backward)
+
+
+def _mutated_decode(old, new):
+    """A copy of oracle.decode.ring_decode_fwd with one source fragment replaced."""
+    import inspect
+    from oracle import decode as D
+    src = inspect.getsource(D.ring_decode_fwd)
+    assert old in src
+    ns = dict(vars(D))
+    exec(src.replace(old, new), ns)
+    return ns["ring_decode_fwd"]
+
+
+def test_decode_queries_at_the_start_are_caught(monkeypatch):
+    from oracle import decode as D
+    import tests.test_oracle_decode as TD
+    monkeypatch.setattr(D, "ring_decode_fwd", _mutated_decode("np.arange(S - Tq, S)", "np.arange(0, Tq)"))
+    _fails(TD.test_single_query_sees_its_own_key_last)
+    _fails(TD.test_zero_query_gives_visible_mean)
+
+
+def test_decode_missing_rescale_is_caught(monkeypatch):
+    from oracle import decode as D
+    import tests.test_oracle_decode as TD
+    monkeypatch.setattr(D, "ring_decode_fwd", _mutated_decode("num = num * corr[..., None] +", "num = num +"))
+    _fails(TD.test_matches_torch_sdpa_fp64, 64, 4, 5, True)
