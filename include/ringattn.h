@@ -142,6 +142,29 @@ int ring_attn_fwd_ordered(const void* q, const void* k, const void* v, void* o, 
                           const int* kv_order, hipStream_t stream);
 
 /*
+ * Ring decode (the paper's appendix on the inference requirement), bf16: the Tq newest
+ * tokens attend to a key/value cache of S tokens that stays split in n_hosts blocks of
+ * c = S / n_hosts over the ring.  The queries sit at global positions S - Tq .. S - 1
+ * (their own keys and values are the last Tq rows of the cache) on the last host, and the
+ * blocks are folded into their running maximum / numerator / denominator in ring order,
+ * block n_hosts-1 first, then n_hosts-2, ..., 0 (Section 3), with the online-softmax
+ * recurrence of Section 2.  With causal != 0 query t sees cache positions <= S - Tq + t;
+ * otherwise the whole cache.  On one GPU all blocks are resident: one launch computes the
+ * partial state of every block (each split in chunks, one wave per chunk; the step reads
+ * the whole cache once and is bound by HBM bandwidth) and a second folds them in ring
+ * order.
+ *   q        in   bf16 [B, Tq, H, D]
+ *   k_cache, v_cache in bf16 [B, S, H, D]
+ *   o        out  bf16 [B, Tq, H, D]
+ *   lse      out  f32  [B, H, Tq]      max + ln(denominator) of each query's scaled scores
+ *   1 <= Tq <= min(32, S); D in {64, 128}; S % n_hosts == 0 and c a multiple of 32;
+ *   n_hosts <= 64.  Workspace: B * H * (S / chunk) * Tq * (D + 2) floats, stream-ordered.
+ */
+int ring_attn_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
+                     int B, int H, int S, int D, int Tq, int n_hosts, int causal,
+                     hipStream_t stream);
+
+/*
  * Blockwise feed-forward network (Section 2 equation and "Blockwise Parallel
  * Transformers"; Algorithm 1's feed-forward step), bf16:
  *   y = act(x W1 + b1) W2 + b2, computed `block` rows at a time, so the [rows, d_ff]
@@ -217,7 +240,7 @@ const char* ring_attn_last_error(void);
  * waits for the recorded launches of that kind, returns their summed duration in
  * milliseconds and their number, and forgets them.  Kinds:
  */
-enum { RA_KERNEL_ATTN_FWD = 0, RA_KERNEL_ATTN_BWD = 1, RA_KERNEL_GEMM = 2 };
+enum { RA_KERNEL_ATTN_FWD = 0, RA_KERNEL_ATTN_BWD = 1, RA_KERNEL_GEMM = 2, RA_KERNEL_DECODE = 3 };
 void ring_attn_timing_enable(int on);
 int ring_attn_timing_read(int kind, double* total_ms, int* launches);
 

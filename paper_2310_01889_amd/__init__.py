@@ -18,9 +18,10 @@ import torch
 __all__ = [
     "RingAttnError", "library_path", "load", "exported_symbols",
     "ring_attn_fwd", "ring_attn_bwd", "ring_attn_fwd_f32", "ring_attn_bwd_f32",
-    "ring_attn_fwd_host", "ring_attn_bwd_host", "ring_attn_fwd_ordered", "blockwise_ffn", "blockwise_ffn_bwd",
+    "ring_attn_fwd_host", "ring_attn_bwd_host", "ring_attn_fwd_ordered", "ring_attn_decode",
+    "blockwise_ffn", "blockwise_ffn_bwd",
     "blockwise_linear", "blockwise_linear_bwd", "ring_layer_fwd", "ring_layer_bwd",
-    "attention_fwd", "attention_bwd",
+    "attention_fwd", "attention_bwd", "attention_decode",
     "ACT_GELU_ERF", "ACT_RELU", "ACT_GELU_TANH",
 ]
 
@@ -38,6 +39,7 @@ _SIGS = {
     "ring_attn_fwd_host": [_P] * 5 + [_I] * 7 + [_P],
     "ring_attn_bwd_host": [_P] * 9 + [_I] * 7 + [_P],
     "ring_attn_fwd_ordered": [_P] * 5 + [_I] * 6 + [_P, _P],
+    "ring_attn_decode": [_P] * 5 + [_I] * 7 + [_P],
     "blockwise_ffn": [_P] * 6 + [_I] * 5 + [_P],
     "blockwise_ffn_bwd": [_P] * 10 + [_I] * 5 + [_P],
     "blockwise_linear": [_P] * 4 + [_I] * 4 + [_P],
@@ -91,7 +93,7 @@ def exported_symbols():
                                  "ring_attn_timing_read"])
 
 
-KERNEL_ATTN_FWD, KERNEL_ATTN_BWD, KERNEL_GEMM = 0, 1, 2
+KERNEL_ATTN_FWD, KERNEL_ATTN_BWD, KERNEL_GEMM, KERNEL_DECODE = 0, 1, 2, 3
 
 
 def timing_enable(on=True):
@@ -202,6 +204,15 @@ def ring_attn_fwd_ordered(q, k, v, o, lse, n_hosts, causal, kv_order, stream=Non
           ctypes.cast(arr, ctypes.c_void_p), _stream(stream))
 
 
+def ring_attn_decode(q, k_cache, v_cache, o, lse, n_hosts, causal=True, stream=None):
+    B, Tq, H, D = _bshd(q)
+    S = int(k_cache.shape[1])
+    bf = torch.bfloat16
+    _call("ring_attn_decode", _ptr(q, bf, "q"), _ptr(k_cache, bf, "k_cache"), _ptr(v_cache, bf, "v_cache"),
+          _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"), B, H, S, D, Tq, int(n_hosts), int(causal),
+          _stream(stream))
+
+
 def blockwise_ffn(x, w1, b1, w2, b2, y, block, act=ACT_GELU_ERF, stream=None):
     T, dm = (int(s) for s in x.shape)
     dff = int(w1.shape[1])
@@ -274,3 +285,12 @@ def attention_bwd(q, k, v, o, lse, dO, n_hosts, causal=True):
     fn = ring_attn_bwd if q.dtype == torch.bfloat16 else ring_attn_bwd_f32
     fn(q, k, v, o, lse, dO, dq, dk, dv, n_hosts, causal)
     return dq, dk, dv
+
+
+def attention_decode(q, k_cache, v_cache, n_hosts, causal=True):
+    """Returns (o [B, Tq, H, D] bf16, lse [B, H, Tq] f32) of ring_attn_decode."""
+    B, Tq, H, D = _bshd(q)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, Tq), dtype=torch.float32, device=q.device)
+    ring_attn_decode(q, k_cache, v_cache, o, lse, n_hosts, causal)
+    return o, lse

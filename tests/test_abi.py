@@ -66,6 +66,22 @@ def test_attention_argument_validation(lib):
                              1, 1, 1024, 128, 4, 1, NULL) == RA_EINVAL
 
 
+def test_decode_argument_validation(lib):
+    def dec(*, q=FAKE, B=1, H=2, S=4096, D=128, Tq=1, N=8, causal=1):
+        return lib.ring_attn_decode(q, FAKE, FAKE, FAKE, FAKE, B, H, S, D, Tq, N, causal, NULL)
+    assert dec(q=NULL) == RA_EINVAL
+    assert dec(Tq=0) == RA_EINVAL
+    assert dec(S=16, N=1, Tq=17) == RA_EINVAL            # more queries than cache
+    assert dec(causal=-1) == RA_EINVAL
+    assert dec(Tq=33) == RA_EUNSUPPORTED                 # at most 32 query tokens
+    assert b"32" in lib.ring_attn_last_error()
+    assert dec(D=80) == RA_EUNSUPPORTED
+    assert dec(S=4096, N=3) == RA_EUNSUPPORTED           # S % n_hosts
+    assert dec(S=4096 + 16 * 8, N=8) == RA_EUNSUPPORTED  # block 528 not a multiple of 32
+    assert dec(N=65, S=65 * 64) == RA_EUNSUPPORTED
+    assert dec(B=1 << 10, H=64, S=1 << 16, N=8) == RA_EUNSUPPORTED
+
+
 def test_ffn_argument_validation(lib):
     f = lib.blockwise_ffn
     assert f(FAKE, FAKE, NULL, FAKE, NULL, FAKE, 512, 256, 512, 256, 5, NULL) == RA_EINVAL
