@@ -15,7 +15,8 @@ masking halves the diagonal blocks and skips blocks above the diagonal).  The
 launch, on the stream it runs on) against the bf16 dense matrix-core peak.  The
 `cpu_baseline` object times the fp64 CPU oracle on one head of the same workload and
 scales it to all 32 heads.  `extra` holds secondary configurations measured in the same
-run (forward+backward at S=16384, one host's share at 262144 tokens) for context.
+run (forward+backward at S=16384, one host's share at 262144 tokens, ring decode of 1 and 8
+tokens against a 262144-token cache, blockwise FFN and the full layer) for context.
 """
 import argparse
 import json
@@ -185,6 +186,26 @@ def main():
         f5 = 4.0 * H5 * D * host_pairs(c5, 7, N5)
         extra["host7_of_8_c32768_H32"] = {"ms": round(ms5, 3), "tflops": round(f5 / ms5 / 1e9, 2),
                                           "query_tokens_per_s": round(c5 / (ms5 * 1e-3), 1)}
+        # ring decode against the same 262144-token cache (8 hosts x 32768), 1 and 8 new tokens
+        for tq in (1, 8):
+            qd = mk(1, tq, H5, D)
+            od = torch.empty_like(qd)
+            ld = torch.empty((1, H5, tq), dtype=torch.float32, device="cuda")
+            dec = lambda: ra.ring_attn_decode(qd, k5, v5, od, ld, N5, True)
+            for _ in range(3):
+                dec()
+            torch.cuda.synchronize()
+            ra.timing_read(ra.KERNEL_DECODE)
+            ra.timing_enable(True)
+            msd, _ = time_calls(dec, 20, 0)
+            ra.timing_enable(False)
+            kd, nd = ra.timing_read(ra.KERNEL_DECODE)
+            kv_bytes = 2.0 * N5 * c5 * H5 * D * 2
+            extra["decode_S262144_H32_Tq%d" % tq] = {
+                "ms": round(msd, 4), "partial_kernel_ms": round(kd / nd, 4),
+                "kv_GBps": round(kv_bytes / (kd / nd) / 1e6, 1),
+                "pct_hbm_8TBps": round(100.0 * kv_bytes / (kd / nd) / 1e6 / 8000.0, 1),
+                "tokens_per_s": round(tq / (msd * 1e-3), 1)}
         del qb, k5, v5, ob, lb
         # blockwise FFN and the full layer (forward + backward) at d_model 4096, d_ff 16384,
         # S = 65536 in 8 host blocks of 8192, 32 heads of 128

@@ -11,8 +11,8 @@
 // On one GPU every block is resident, so one launch computes the partial state of every
 // block at once, each block split into chunks of `kch` keys for parallelism (one wave per
 // (batch, head, chunk)): the step is a read of the whole cache, bound by HBM bandwidth.
-// A second launch folds the partial states of each (batch, head, query) in ring order,
-// block by block and, inside a block, chunk by chunk, and writes o and lse.
+// A second launch combines the partial states of each (batch, head, query) in ring
+// order, block by block and, inside a block, chunk by chunk, and writes o and lse.
 #include "ra_common.h"
 #include "ra_runtime.h"
 #include "ringattn.h"
@@ -220,10 +220,13 @@ struct MergeArgs {
   int B, H, Tq, nch, n_hosts;
 };
 
-// One workgroup of 64 threads per (batch, head, query): fold the chunk partial states
-// in ring order -- blocks n_hosts-1, n_hosts-2, ..., 0, chunks of a block in order --
-// with the online-softmax combination, then o = numerator / denominator and
-// lse = max + ln(denominator) (natural log).
+// One workgroup of 64 threads per (batch, head, query): combine the chunk partial
+// states in ring order -- blocks n_hosts-1, n_hosts-2, ..., 0, chunks of a block in
+// order.  All partials are present, so instead of carrying a running maximum the sum is
+// taken relative to the overall maximum M (found first, in any order):
+//   o = sum_c acc_c 2^(m_c - M) / sum_c l_c 2^(m_c - M),  lse = (M ln 2) + ln(denominator),
+// which is the online-softmax fold of the same partials in the same order, without its
+// sequential dependence; the loads of all chunks can then be in flight together.
 template <int D>
 __global__ __launch_bounds__(64) void decode_merge_kernel(const MergeArgs a) {
   constexpr int E = D / 64;  // dims per thread
@@ -231,29 +234,31 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(const MergeArgs a) {
   const int b = bh / a.H, h = bh % a.H;
   const int lane = threadIdx.x;
   const int cpb = a.nch / a.n_hosts;  // chunks per block
-  float m = -INFINITY, l = 0.f, acc[E];
+  const long long base = (long long)bh * a.nch;
+  float mx = -INFINITY;
+  for (int c = lane; c < a.nch; c += 64) mx = fmaxf(mx, a.part_m[(base + c) * a.Tq + t]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  float l = 0.f, acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
   for (int step = 0; step < a.n_hosts; ++step) {
     const int blk = a.n_hosts - 1 - step;
+#pragma unroll 4
     for (int c = 0; c < cpb; ++c) {
-      const long long row = ((long long)bh * a.nch + blk * cpb + c) * a.Tq + t;
-      const float mc = a.part_m[row], lc = a.part_l[row];
-      const float mn = fmaxf(m, mc);
-      if (mn == -INFINITY) continue;  // nothing visible yet
-      const float al = (m == -INFINITY) ? 0.f : exp2f(m - mn);
-      const float be = (mc == -INFINITY) ? 0.f : exp2f(mc - mn);
-      l = l * al + lc * be;
+      const long long row = (base + blk * cpb + c) * a.Tq + t;
+      const float mc = a.part_m[row];
+      const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - mx);
+      l = fmaf(a.part_l[row], w, l);
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = acc[e] * al + a.part_acc[row * D + lane + 64 * e] * be;
-      m = mn;
+      for (int e = 0; e < E; ++e) acc[e] = fmaf(a.part_acc[row * D + lane + 64 * e], w, acc[e]);
     }
   }
   const float inv = 1.f / l;
   bf16* orow = a.o + ((long long)b * a.Tq + t) * a.H * D + h * D;
 #pragma unroll
   for (int e = 0; e < E; ++e) orow[lane + 64 * e] = (bf16)(acc[e] * inv);
-  if (lane == 0) a.lse[(long long)bh * a.Tq + t] = m * kLn2 + logf(l);
+  if (lane == 0) a.lse[(long long)bh * a.Tq + t] = mx * kLn2 + logf(l);
 }
 
 // Keys per chunk: the whole block, halved while the launch has fewer than 4096
