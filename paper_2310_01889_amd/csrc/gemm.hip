@@ -10,13 +10,16 @@
 // epilogues then read bias / residual / pre-activation and write C with vector accesses.
 #include "ra_common.h"
 #include "ra_gemm.h"
+#include "ringattn.h"
 
 namespace ra {
 namespace {
 
 constexpr int kTM = 256, kTN = 256, kTK = 64, kGT = 256;
 
-__device__ __forceinline__ float act_apply(int act, float h) {
+template <int ACT>
+__device__ __forceinline__ float act_apply(float h) {
+  constexpr int act = ACT;
   if (act == 1) return fmaxf(h, 0.f);
   if (act == 2) {
     const float u = 0.7978845608028654f * (h + 0.044715f * h * h * h);
@@ -25,7 +28,9 @@ __device__ __forceinline__ float act_apply(int act, float h) {
   return 0.5f * h * (1.f + erff(h * 0.7071067811865476f));
 }
 
-__device__ __forceinline__ float act_grad(int act, float h) {
+template <int ACT>
+__device__ __forceinline__ float act_grad(float h) {
+  constexpr int act = ACT;
   if (act == 1) return h > 0.f ? 1.f : 0.f;
   if (act == 2) {
     const float u = 0.7978845608028654f * (h + 0.044715f * h * h * h);
@@ -48,7 +53,9 @@ struct TileShape {
   static constexpr int B_CHUNKS = B_ROWS * B_COLS / 8 / kGT;
 };
 
-template <bool TA, bool TB, int EPI>
+// ACT: the activation of the ACT epilogues (an ra_act value, fixed at compile time so
+// that each kernel holds the code of one activation only).
+template <bool TA, bool TB, int EPI, int ACT>
 __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
   using TS = TileShape<TA, TB>;
   extern __shared__ __attribute__((aligned(16))) bf16 smem[];
@@ -180,7 +187,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
           if (EPI == EPI_ACT_STORE_H) *(f32x4*)(g.aux_f32 + off) = f32x4{v[0], v[1], v[2], v[3]};
           if (EPI != EPI_BF16) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = act_apply(g.act, v[e]);
+            for (int e = 0; e < 4; ++e) v[e] = act_apply<ACT>(v[e]);
           }
           if (g.residual) {
             const bf16x4 rr = *(const bf16x4*)((const bf16*)g.residual + off);
@@ -191,7 +198,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
         } else if (EPI == EPI_ACT_GRAD_BF16) {
           const f32x4 h = *(const f32x4*)(g.aux_f32 + off);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] *= act_grad(g.act, h[e]);
+          for (int e = 0; e < 4; ++e) v[e] *= act_grad<ACT>(h[e]);
           *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
         } else {  // EPI_F32: overwrite, or add into C
           f32x4* cp = (f32x4*)((float*)g.C + off);
@@ -228,16 +235,16 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* part, fl
   out[n] = accumulate ? out[n] + s : s;
 }
 
-template <bool TA, bool TB, int EPI>
+template <bool TA, bool TB, int EPI, int ACT>
 hipError_t launch_t(const GemmArgs& g, hipStream_t st) {
   using TS = TileShape<TA, TB>;
   const size_t lds = (size_t)(2 * TS::A_ELEMS + 2 * TS::B_ELEMS) * sizeof(bf16);
   // the tiles need more than the default dynamic LDS limit (set on the current device)
-  hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<TA, TB, EPI>,
+  hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<TA, TB, EPI, ACT>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const int total = (g.M / kTM) * (g.N / kTN);
-  hipLaunchKernelGGL((gemm_kernel<TA, TB, EPI>), dim3(total), dim3(kGT), lds, st, g);
+  hipLaunchKernelGGL((gemm_kernel<TA, TB, EPI, ACT>), dim3(total), dim3(kGT), lds, st, g);
   return hipGetLastError();
 }
 
@@ -246,15 +253,22 @@ hipError_t launch_t(const GemmArgs& g, hipStream_t st) {
 hipError_t launch_gemm(const GemmArgs& g, bool ta, bool tb, int epi, hipStream_t st) {
   if (g.M % kTM || g.N % kTN || g.K % kTK) return hipErrorInvalidValue;
 #define RA_GEMM_CASE(TA_, TB_, E_) \
-  if (ta == TA_ && tb == TB_ && epi == E_) return launch_t<TA_, TB_, E_>(g, st);
+  if (ta == TA_ && tb == TB_ && epi == E_) return launch_t<TA_, TB_, E_, 0>(g, st);
+#define RA_GEMM_CASE_ACT(TA_, TB_, E_)                                                 \
+  if (ta == TA_ && tb == TB_ && epi == E_) {                                           \
+    if (g.act == RA_ACT_RELU) return launch_t<TA_, TB_, E_, RA_ACT_RELU>(g, st);       \
+    if (g.act == RA_ACT_GELU_TANH) return launch_t<TA_, TB_, E_, RA_ACT_GELU_TANH>(g, st); \
+    return launch_t<TA_, TB_, E_, RA_ACT_GELU_ERF>(g, st);                             \
+  }
   RA_GEMM_CASE(false, false, EPI_BF16)
-  RA_GEMM_CASE(false, false, EPI_ACT_BF16)
-  RA_GEMM_CASE(false, false, EPI_ACT_STORE_H)
+  RA_GEMM_CASE_ACT(false, false, EPI_ACT_BF16)
+  RA_GEMM_CASE_ACT(false, false, EPI_ACT_STORE_H)
   RA_GEMM_CASE(false, true, EPI_BF16)
-  RA_GEMM_CASE(false, true, EPI_ACT_GRAD_BF16)
+  RA_GEMM_CASE_ACT(false, true, EPI_ACT_GRAD_BF16)
   RA_GEMM_CASE(true, false, EPI_F32)
   RA_GEMM_CASE(false, true, EPI_F32)
 #undef RA_GEMM_CASE
+#undef RA_GEMM_CASE_ACT
   return hipErrorInvalidValue;
 }
 
