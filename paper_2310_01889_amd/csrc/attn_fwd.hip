@@ -241,6 +241,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[mt][i]);
     rescale(mx, sc);
   };
+  auto mask_half = [&](f32x16* sc, int mt, int it) __attribute__((always_inline)) {
+    const int kpos0 = hs.k_pos0 + it * kBN;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
+      if (kpos > qpos) sc[mt][i] = -INFINITY;
+    }
+  };
   auto mask = [&](f32x16* sc, int it) __attribute__((always_inline)) {
     const int kpos0 = hs.k_pos0 + it * kBN;
 #pragma unroll
@@ -311,9 +319,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     uint32_t w[4][4];
     float rs2[4] = {0.f, 0.f, 0.f, 0.f};
     float mxa = -INFINITY, mxb = -INFINITY;
+    // score MFMA S: the two 32-key halves alternate (mt = S % 2, kk = S / 2), so that
+    // consecutive score MFMAs are independent
     auto read_k = [&](auto Sc) __attribute__((always_inline)) {
-      constexpr int S = decltype(Sc)::value;  // score MFMA S: mt = S / 8, kk = S % 8
-      kop[S] = *(const bf16x8*)(kt + 32 * (S / NKK) * D + koff[S % NKK]);
+      constexpr int S = decltype(Sc)::value;
+      kop[S] = *(const bf16x8*)(kt + 32 * (S % 2) * D + koff[S / 2]);
     };
     auto read_v = [&](auto Sc) __attribute__((always_inline)) {
       constexpr int S = decltype(Sc)::value;  // PV MFMA S: kb = S / NDT, dt = S % NDT
@@ -321,33 +331,49 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       const bf16x4 up = lds_read_tr16(vt + 16 * (S / NDT) * D + voff[1][S % NDT]);
       vop[S] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
     };
+    // 21 steps.  Step S: score MFMA S (S < 16); PV MFMA S - 5 (S >= 5); the exponentials of
+    // pair S (S < 16), the bf16 packing of pair S - 1 and the row-sum update of pair S - 2,
+    // so that no step waits on a result of its own; the next tile's masking and maximum
+    // from step 16 on (the last score MFMAs issue at steps 14 and 15).
+    float pe0[16], pe1[16];
+    constexpr int kPVD = 5;
     static_for<0, kPF>([&](auto Sc) __attribute__((always_inline)) { read_k(Sc); });
-    static_for<0, 20>([&](auto Sc) __attribute__((always_inline)) {
+    static_for<0, 16 + kPVD>([&](auto Sc) __attribute__((always_inline)) {
       constexpr int S = decltype(Sc)::value;
       if constexpr (S + kPF < 16) read_k(std::integral_constant<int, S + kPF>{});
-      if constexpr (S + kPF >= 4 && S + kPF < 20) read_v(std::integral_constant<int, S + kPF - 4>{});
+      if constexpr (S + kPF >= kPVD && S + kPF < 16 + kPVD) read_v(std::integral_constant<int, S + kPF - kPVD>{});
       if constexpr (S < 16) {
-        constexpr int mt = S / NKK, kk = S % NKK;
+        constexpr int mt = S % 2, kk = S / 2;
         s_next[mt] = mfma32(kop[S], qreg[kk], kk == 0 ? minit : s_next[mt]);
       }
-      if constexpr (S >= 4) {
-        constexpr int q = S - 4, kb = q / NDT, dt = q % NDT;
+      if constexpr (S >= kPVD) {
+        constexpr int q = S - kPVD, kb = q / NDT, dt = q % NDT;
         if constexpr (dt == 0) pb[kb] = __builtin_bit_cast(bf16x8, u32x4{w[kb][0], w[kb][1], w[kb][2], w[kb][3]});
         oacc[dt] = mfma32(vop[q], pb[kb], oacc[dt]);
       }
       if constexpr (S < 16) {
         constexpr int kb = S / 4, j = S % 4;
-        const float p0 = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j]);
-        const float p1 = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
-        w[kb][j] = pack_bf16x2(p0, p1);
-        rs2[j] = dot2_bf16_ones(w[kb][j], rs2[j]);  // row sum of the bf16 probabilities used
-      } else if constexpr (S < 18) {
-        if constexpr (S == 16 && MN) mask(s_next, it + 1);
+        pe0[S] = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j]);
+        pe1[S] = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
+      }
+      if constexpr (S >= 1 && S <= 16) {
+        constexpr int P = S - 1;
+        w[P / 4][P % 4] = pack_bf16x2(pe0[P], pe1[P]);
+      }
+      if constexpr (S >= 2 && S <= 17) {
+        constexpr int P = S - 2;
+        rs2[P % 4] = dot2_bf16_ones(w[P / 4][P % 4], rs2[P % 4]);  // row sum of the bf16 probabilities used
+      }
+      if constexpr (S == 16 || S == 17) {
+        if constexpr (S == 16 && MN) mask_half(s_next, 0, it + 1);
 #pragma unroll
         for (int i = 8 * (S - 16); i < 8 * (S - 15); ++i) mxa = fmaxf(mxa, s_next[0][i]);
-      } else {
+      } else if constexpr (S >= 18) {
+        if constexpr (S == 18 && MN) mask_half(s_next, 1, it + 1);
+        if constexpr (S < 20) {
 #pragma unroll
-        for (int i = 8 * (S - 18); i < 8 * (S - 17); ++i) mxb = fmaxf(mxb, s_next[1][i]);
+          for (int i = 8 * (S - 18); i < 8 * (S - 17); ++i) mxb = fmaxf(mxb, s_next[1][i]);
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     });
