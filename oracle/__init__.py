@@ -23,6 +23,10 @@ Modules
                 at the end of a long key/value cache that is split in host blocks; the
                 blocks circulate past the queries in ring order and are folded into
                 their running softmax state.
+  llama      -- the LLaMA-style layer the paper trains (RMSNorm, rotary position
+                embedding, SwiGLU feed-forward, pre-norm residuals) around the same
+                attention, its backward, and a stack of layers trained with full
+                recomputation.
   layer      -- one transformer layer as Algorithm 1 composes it: projections,
                 ring attention, output projection with residual, blockwise FFN with
                 residual; forward and backward.
@@ -34,5 +38,6 @@ Parity status: attention forward/backward, ring bookkeeping, ring decode and FFN
 tests in tests/test_oracle_*.py (closed forms, invariants, brute force, finite
 differences, library routines).  The layer composition is pinned only to the
 composition defined in ``layer`` (the paper does not fix norms, biases or the
-activation of that layer): for it, parity unpinned beyond its parts.
+activation of that layer), and likewise the composition in ``llama``: for them, parity
+unpinned beyond their parts (each part is pinned).
 """

@@ -1,0 +1,126 @@
+"""Pins for the LLaMA-style layer oracle (CPU only).
+
+RMSNorm against torch's rms_norm and autograd; RoPE against complex multiplication by
+e^{i angle} (torch.polar on interleaved pairs), the identity at position 0, norm
+preservation, the relative-position property <R_m q, R_n k> = <R_{m-n} q, k> and its
+inverse; SwiGLU's activation against torch.nn.functional.silu and autograd; the layer and
+the stack backward against central finite differences.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import llama as L
+
+
+def _rand(seed, *shape, scale=1.0):
+    return np.random.default_rng(seed).standard_normal(shape) * scale
+
+
+def test_rmsnorm_matches_torch_and_autograd():
+    x, g, dy = _rand(1, 7, 16), _rand(2, 16), _rand(3, 7, 16)
+    y, rstd = L.rmsnorm_fwd(x, g)
+    tx = torch.from_numpy(x).requires_grad_()
+    tg = torch.from_numpy(g).requires_grad_()
+    ty = torch.nn.functional.rms_norm(tx, (16,), weight=tg, eps=L.EPS)
+    np.testing.assert_allclose(y, ty.detach().numpy(), atol=1e-13)
+    np.testing.assert_allclose(rstd, 1.0 / np.sqrt((x * x).mean(1) + L.EPS), atol=1e-13)
+    ty.backward(torch.from_numpy(dy))
+    dx, dg = L.rmsnorm_bwd(x, g, dy)
+    np.testing.assert_allclose(dx, tx.grad.numpy(), atol=1e-12)
+    np.testing.assert_allclose(dg, tg.grad.numpy(), atol=1e-12)
+
+
+def test_rope_is_complex_rotation():
+    x = _rand(4, 5, 3, 8)
+    pos = np.array([0, 1, 7, 100, 65535])
+    y = L.rope(x, pos)
+    xc = torch.view_as_complex(torch.from_numpy(x).reshape(5, 3, 4, 2).contiguous())
+    ang = torch.from_numpy(L.rope_angles(pos, 8))[:, None, :]
+    rot = torch.polar(torch.ones_like(ang), ang)
+    ref = torch.view_as_real(xc * rot).reshape(5, 3, 8).numpy()
+    np.testing.assert_allclose(y, ref, atol=1e-12)
+    np.testing.assert_allclose(L.rope_angles([1], 2)[0, 0], 1.0)  # theta_0 = base^0
+
+
+def test_rope_properties():
+    q, k = _rand(5, 1, 2, 16), _rand(6, 1, 2, 16)
+    np.testing.assert_allclose(L.rope(q, [0]), q, atol=0)  # identity at position 0
+    y = L.rope(q, [12345])
+    pair_norm = lambda t: t[..., 0::2] ** 2 + t[..., 1::2] ** 2
+    np.testing.assert_allclose(pair_norm(y), pair_norm(q), atol=1e-12)
+    # relative position: <R_m q, R_n k> = <R_{m-n} q, k>
+    for m, n in ((9, 4), (300, 299), (5, 40)):
+        lhs = (L.rope(q, [m]) * L.rope(k, [n])).sum(-1)
+        rhs = (L.rope(q, [m - n]) * k).sum(-1)
+        np.testing.assert_allclose(lhs, rhs, atol=1e-11)
+    np.testing.assert_allclose(L.rope(y, [12345], inverse=True), q, atol=1e-12)
+
+
+def test_silu_matches_torch():
+    u = np.linspace(-12, 12, 97)
+    tu = torch.from_numpy(u).requires_grad_()
+    ts = torch.nn.functional.silu(tu)
+    np.testing.assert_allclose(L.silu(u), ts.detach().numpy(), atol=1e-14)
+    ts.sum().backward()
+    np.testing.assert_allclose(L.silu_grad(u), tu.grad.numpy(), atol=1e-14)
+
+
+def test_swiglu_backward_matches_autograd():
+    x, w1, w3, w2, dy = _rand(7, 5, 8), _rand(8, 8, 12), _rand(9, 8, 12), _rand(10, 12, 8), _rand(11, 5, 8)
+    ts = [torch.from_numpy(t).requires_grad_() for t in (x, w1, w3, w2)]
+    out = (torch.nn.functional.silu(ts[0] @ ts[1]) * (ts[0] @ ts[2])) @ ts[3]
+    np.testing.assert_allclose(L.swiglu_fwd(x, w1, w3, w2), out.detach().numpy(), atol=1e-12)
+    out.backward(torch.from_numpy(dy))
+    for mine, t in zip(L.swiglu_bwd(x, w1, w3, w2, dy), ts):
+        np.testing.assert_allclose(mine, t.grad.numpy(), atol=1e-11)
+
+
+def _tiny_layer(seed, S=6, d=8, dff=6):
+    r = np.random.default_rng(seed)
+    w = lambda *s: r.standard_normal(s) * 0.3
+    return (r.standard_normal((S, d)), 1.0 + 0.1 * r.standard_normal(d), w(d, d), w(d, d), w(d, d), w(d, d),
+            1.0 + 0.1 * r.standard_normal(d), w(d, dff), w(d, dff), w(dff, d)), r.standard_normal((S, d))
+
+
+def _fd(loss, arrays, idx, eps=1e-6):
+    a = arrays[idx]
+    num = np.zeros_like(a)
+    for pos in np.ndindex(a.shape):
+        old = a[pos]
+        a[pos] = old + eps
+        lp = loss()
+        a[pos] = old - eps
+        lm = loss()
+        a[pos] = old
+        num[pos] = (lp - lm) / (2 * eps)
+    return num
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_layer_backward_finite_differences(causal):
+    params, dz = _tiny_layer(12)
+    arrays = [p.copy() for p in params]
+    H = 2
+    loss = lambda: float((L.layer_fwd(*arrays, H, causal) * dz).sum())
+    grads = L.layer_bwd(*arrays, dz, H, causal)
+    for idx in range(len(arrays)):  # x, g1, wq, wk, wv, wo, g2, w1, w3, w2
+        np.testing.assert_allclose(grads[idx], _fd(loss, arrays, idx), atol=2e-7, rtol=1e-6)
+
+
+def test_stack_backward_finite_differences():
+    p1, dz = _tiny_layer(13)
+    p2, _ = _tiny_layer(14)
+    x = p1[0].copy()
+    layers = [list(p1[1:]), list(p2[1:])]
+    loss = lambda: float((L.stack_fwd(x, layers, 2) * dz).sum())
+    dx, grads = L.stack_bwd(x, layers, dz, 2)
+    np.testing.assert_allclose(dx, _fd(loss, [x], 0), atol=2e-7, rtol=1e-6)
+    for li in range(2):
+        for pi in (0, 3, 6, 8):  # g1, wv, w1, w2 of each layer
+            num = _fd(loss, layers[li], pi)
+            np.testing.assert_allclose(grads[li][pi], num, atol=2e-7, rtol=1e-6)
+    # one layer: the stack is the layer
+    dx1, g1 = L.stack_bwd(x, layers[:1], dz, 2)
+    ref = L.layer_bwd(x, *layers[0], dz, 2)
+    np.testing.assert_allclose(dx1, ref[0], atol=1e-13)

@@ -106,3 +106,35 @@ def test_decode_missing_rescale_is_caught(monkeypatch):
     import tests.test_oracle_decode as TD
     monkeypatch.setattr(D, "ring_decode_fwd", _mutated_decode("num = num * corr[..., None] +", "num = num +"))
     _fails(TD.test_matches_torch_sdpa_fp64, 64, 4, 5, True)
+
+
+def _mutated(module, fname, old, new):
+    """A copy of module.fname with one source fragment replaced."""
+    import inspect
+    src = inspect.getsource(getattr(module, fname))
+    assert old in src
+    ns = dict(vars(module))
+    exec(src.replace(old, new), ns)
+    return ns[fname]
+
+
+def test_llama_rope_half_split_pairing_is_caught(monkeypatch):
+    from oracle import llama as LL
+    import tests.test_oracle_llama as TL
+    bad = _mutated(LL, "rope", "x0, x1 = x[..., 0::2], x[..., 1::2]", "x0, x1 = x[..., :D // 2], x[..., D // 2:]")
+    monkeypatch.setattr(LL, "rope", bad)
+    _fails(TL.test_rope_is_complex_rotation)
+
+
+def test_llama_rmsnorm_dropped_term_is_caught(monkeypatch):
+    from oracle import llama as LL
+    import tests.test_oracle_llama as TL
+    monkeypatch.setattr(LL, "rmsnorm_bwd", _mutated(LL, "rmsnorm_bwd", "gdy * rstd[:, None] - x *", "gdy * rstd[:, None] - 0 * x *"))
+    _fails(TL.test_rmsnorm_matches_torch_and_autograd)
+
+
+def test_llama_swiglu_wrong_derivative_is_caught(monkeypatch):
+    from oracle import llama as LL
+    import tests.test_oracle_llama as TL
+    monkeypatch.setattr(LL, "swiglu_bwd", _mutated(LL, "swiglu_bwd", "w * silu_grad(u)", "w * silu(u)"))
+    _fails(TL.test_swiglu_backward_matches_autograd)
