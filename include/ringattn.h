@@ -229,6 +229,87 @@ int ring_layer_bwd(const void* x, const void* wq, const void* wk, const void* wv
                    float* dwv, float* dwo, float* dw1, float* dw2, int S, int d_model, int n_heads,
                    int d_ff, int n_hosts, int causal, int act, hipStream_t stream);
 
+/*
+ * LLaMA-style layer (the architecture the paper trains, Section 4 model configuration)
+ * and its pieces.  The pieces are not defined by the paper; these entry points implement
+ * the usual definitions, stated here:
+ *   RMSNorm   y = x / sqrt(mean(x^2) + 1e-6) * g   (row-wise; gain g bf16 [d])
+ *   RoPE      in each head, pair (2i, 2i+1) at global position p rotated by the angle
+ *             p * 10000^(-2i/D)
+ *   SwiGLU    (silu(x W1) * (x W3)) W2,  silu(u) = u / (1 + e^-u)
+ *   layer     n1 = RMSNorm(x; g1);  h = x + Attn(RoPE(n1 Wq), RoPE(n1 Wk), n1 Wv) Wo;
+ *             z = h + SwiGLU(RMSNorm(h; g2))
+ * with Attn the ring attention of this library (causal by global position).
+ */
+
+/* RMSNorm forward.  x in bf16 [T, d]; g in bf16 [d]; y out bf16 [T, d]; rstd out f32 [T]
+ * (1 / sqrt(mean(x^2) + eps)) or NULL.  d % 8 == 0, d <= 8192. */
+int rms_norm_fwd(const void* x, const void* g, void* y, float* rstd, int T, int d, hipStream_t stream);
+
+/* RMSNorm backward for upstream dy (f32 [T, d]): dx out bf16 [T, d] = dres + dx_norm (dres
+ * bf16 [T, d] or NULL: a residual gradient added before the one rounding); dg out f32 [d]
+ * (overwritten; summed over rows in a fixed order). */
+int rms_norm_bwd(const void* x, const void* g, const float* dy, const void* dres, void* dx, float* dg,
+                 int T, int d, hipStream_t stream);
+
+/* Rotary position embedding in place on x bf16 [S, H, D] (rows at global positions
+ * pos0 .. pos0 + S - 1); inverse = 1 applies the transpose (rotation by minus the angle),
+ * which is the backward pass.  D % 4 == 0.  Angles are formed in double precision. */
+int rope_apply(void* x, int S, int H, int D, int pos0, int inverse, hipStream_t stream);
+
+/* SwiGLU feed-forward over row blocks of `block`:
+ *   y = (silu(x W1) * (x W3)) W2 (+ residual)
+ *   x in bf16 [T, d_model]; w1, w3 in bf16 [d_model, d_ff]; w2 in bf16 [d_ff, d_model];
+ *   residual bf16 [T, d_model] or NULL; y out bf16 [T, d_model].  Shapes as blockwise_ffn. */
+int swiglu_ffn(const void* x, const void* w1, const void* w3, const void* w2, const void* residual,
+               void* y, int T, int d_model, int d_ff, int block, hipStream_t stream);
+
+/* Backward of swiglu_ffn (no residual) for upstream dy bf16 [T, d_model], recomputing
+ * x W1 and x W3 block by block: dx out bf16 [T, d_model]; dw1, dw3 out f32 [d_model, d_ff],
+ * dw2 out f32 [d_ff, d_model] (overwritten). */
+int swiglu_ffn_bwd(const void* x, const void* w1, const void* w3, const void* w2, const void* dy,
+                   void* dx, float* dw1, float* dw3, float* dw2, int T, int d_model, int d_ff,
+                   int block, hipStream_t stream);
+
+/*
+ * One LLaMA-style layer, forward (batch 1).
+ *   x       in  bf16 [S, d_model]
+ *   params  HOST array of 9 device pointers, in this order:
+ *           g1 [d_model], wq, wk, wv, wo [d_model, d_model], g2 [d_model],
+ *           w1, w3 [d_model, d_ff], w2 [d_ff, d_model]       (all bf16)
+ *   z       out bf16 [S, d_model]
+ * d_model = n_heads * D with D in {64, 128}, d_model <= 8192; S % n_hosts == 0; the host
+ * block S / n_hosts (the projection and feed-forward block) and d_model, d_ff multiples of 256.
+ */
+int llama_layer_fwd(const void* x, const void* const* params, void* z, int S, int d_model,
+                    int n_heads, int d_ff, int n_hosts, int causal, hipStream_t stream);
+
+/*
+ * Backward of llama_layer_fwd for upstream dz (bf16 [S, d_model]); the forward is
+ * recomputed from x (full gradient checkpointing, the paper's training setting).
+ *   dx     out bf16 [S, d_model]
+ *   grads  HOST array of 9 device pointers (f32, overwritten) matching params:
+ *          dg1, dwq, dwk, dwv, dwo, dg2, dw1, dw3, dw2
+ */
+int llama_layer_bwd(const void* x, const void* const* params, const void* dz, void* dx,
+                    float* const* grads, int S, int d_model, int n_heads, int d_ff, int n_hosts,
+                    int causal, hipStream_t stream);
+
+/*
+ * One training step of a stack of n_layers LLaMA-style layers: the forward pass keeps only
+ * each layer's input, the backward pass runs the layers last to first, each recomputing
+ * its own forward (the paper's full recomputation of attention and feed-forward).
+ *   x       in  bf16 [S, d_model]
+ *   params  HOST array of 9 * n_layers device pointers (layer l at params + 9 l, as above)
+ *   dz      in  bf16 [S, d_model]: gradient of the loss with respect to the stack output
+ *   z       out bf16 [S, d_model]: the stack output
+ *   dx      out bf16 [S, d_model]
+ *   grads   HOST array of 9 * n_layers device pointers (f32, overwritten)
+ */
+int llama_stack_train_step(const void* x, const void* const* params, const void* dz, void* z,
+                           void* dx, float* const* grads, int n_layers, int S, int d_model,
+                           int n_heads, int d_ff, int n_hosts, int causal, hipStream_t stream);
+
 /* Description of the last error returned on the calling thread ("" if none).  Valid
  * until the next library call on that thread. */
 const char* ring_attn_last_error(void);

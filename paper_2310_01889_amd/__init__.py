@@ -21,6 +21,8 @@ __all__ = [
     "ring_attn_fwd_host", "ring_attn_bwd_host", "ring_attn_fwd_ordered", "ring_attn_decode",
     "blockwise_ffn", "blockwise_ffn_bwd",
     "blockwise_linear", "blockwise_linear_bwd", "ring_layer_fwd", "ring_layer_bwd",
+    "rms_norm_fwd", "rms_norm_bwd", "rope_apply", "swiglu_ffn", "swiglu_ffn_bwd",
+    "llama_layer_fwd", "llama_layer_bwd", "llama_stack_train_step",
     "attention_fwd", "attention_bwd", "attention_decode",
     "ACT_GELU_ERF", "ACT_RELU", "ACT_GELU_TANH",
 ]
@@ -46,6 +48,14 @@ _SIGS = {
     "blockwise_linear_bwd": [_P] * 5 + [_I] * 4 + [_P],
     "ring_layer_fwd": [_P] * 8 + [_I] * 7 + [_P],
     "ring_layer_bwd": [_P] * 15 + [_I] * 7 + [_P],
+    "rms_norm_fwd": [_P] * 4 + [_I] * 2 + [_P],
+    "rms_norm_bwd": [_P] * 6 + [_I] * 2 + [_P],
+    "rope_apply": [_P] + [_I] * 5 + [_P],
+    "swiglu_ffn": [_P] * 6 + [_I] * 4 + [_P],
+    "swiglu_ffn_bwd": [_P] * 9 + [_I] * 4 + [_P],
+    "llama_layer_fwd": [_P] * 3 + [_I] * 6 + [_P],
+    "llama_layer_bwd": [_P] * 5 + [_I] * 6 + [_P],
+    "llama_stack_train_step": [_P] * 6 + [_I] * 7 + [_P],
 }
 
 
@@ -264,6 +274,79 @@ def ring_layer_bwd(x, wq, wk, wv, wo, w1, w2, dz, dx, dwq, dwk, dwv, dwo, dw1, d
           _ptr(wo, bf, "wo"), _ptr(w1, bf, "w1"), _ptr(w2, bf, "w2"), _ptr(dz, bf, "dz"), _ptr(dx, bf, "dx"),
           _ptr(dwq, f, "dwq"), _ptr(dwk, f, "dwk"), _ptr(dwv, f, "dwv"), _ptr(dwo, f, "dwo"), _ptr(dw1, f, "dw1"),
           _ptr(dw2, f, "dw2"), S, dm, int(n_heads), dff, int(n_hosts), int(causal), int(act), _stream(stream))
+
+
+def rms_norm_fwd(x, g, y, rstd=None, stream=None):
+    T, d = (int(s) for s in x.shape)
+    bf = torch.bfloat16
+    _call("rms_norm_fwd", _ptr(x, bf, "x"), _ptr(g, bf, "g"), _ptr(y, bf, "y"), _ptr(rstd, torch.float32, "rstd"),
+          T, d, _stream(stream))
+
+
+def rms_norm_bwd(x, g, dy, dres, dx, dg, stream=None):
+    T, d = (int(s) for s in x.shape)
+    bf, f = torch.bfloat16, torch.float32
+    _call("rms_norm_bwd", _ptr(x, bf, "x"), _ptr(g, bf, "g"), _ptr(dy, f, "dy"), _ptr(dres, bf, "dres"),
+          _ptr(dx, bf, "dx"), _ptr(dg, f, "dg"), T, d, _stream(stream))
+
+
+def rope_apply(x, pos0=0, inverse=False, stream=None):
+    """In place on a bf16 [S, H, D] tensor."""
+    S, H, D = (int(s) for s in x.shape)
+    _call("rope_apply", _ptr(x, torch.bfloat16, "x"), S, H, D, int(pos0), int(bool(inverse)), _stream(stream))
+
+
+def swiglu_ffn(x, w1, w3, w2, residual, y, block, stream=None):
+    T, dm = (int(s) for s in x.shape)
+    dff = int(w1.shape[1])
+    bf = torch.bfloat16
+    _call("swiglu_ffn", _ptr(x, bf, "x"), _ptr(w1, bf, "w1"), _ptr(w3, bf, "w3"), _ptr(w2, bf, "w2"),
+          _ptr(residual, bf, "residual"), _ptr(y, bf, "y"), T, dm, dff, int(block), _stream(stream))
+
+
+def swiglu_ffn_bwd(x, w1, w3, w2, dy, dx, dw1, dw3, dw2, block, stream=None):
+    T, dm = (int(s) for s in x.shape)
+    dff = int(w1.shape[1])
+    bf, f = torch.bfloat16, torch.float32
+    _call("swiglu_ffn_bwd", _ptr(x, bf, "x"), _ptr(w1, bf, "w1"), _ptr(w3, bf, "w3"), _ptr(w2, bf, "w2"),
+          _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"), _ptr(dw1, f, "dw1"), _ptr(dw3, f, "dw3"), _ptr(dw2, f, "dw2"),
+          T, dm, dff, int(block), _stream(stream))
+
+
+def _ptr_array(ts, dtype, name):
+    arr = (ctypes.c_void_p * len(ts))(*[_ptr(t, dtype, name).value for t in ts])
+    return arr, ctypes.cast(arr, ctypes.c_void_p)
+
+
+def llama_layer_fwd(x, params, z, n_heads, n_hosts, causal=True, stream=None):
+    """params: [g1, wq, wk, wv, wo, g2, w1, w3, w2] (bf16 tensors)."""
+    S, dm = (int(s) for s in x.shape)
+    dff = int(params[6].shape[1])
+    keep, parr = _ptr_array(params, torch.bfloat16, "params")
+    _call("llama_layer_fwd", _ptr(x, torch.bfloat16, "x"), parr, _ptr(z, torch.bfloat16, "z"), S, dm, int(n_heads),
+          dff, int(n_hosts), int(causal), _stream(stream))
+
+
+def llama_layer_bwd(x, params, dz, dx, grads, n_heads, n_hosts, causal=True, stream=None):
+    """grads: [dg1, dwq, dwk, dwv, dwo, dg2, dw1, dw3, dw2] (float32 tensors, overwritten)."""
+    S, dm = (int(s) for s in x.shape)
+    dff = int(params[6].shape[1])
+    bf = torch.bfloat16
+    keep_p, parr = _ptr_array(params, bf, "params")
+    keep_g, garr = _ptr_array(grads, torch.float32, "grads")
+    _call("llama_layer_bwd", _ptr(x, bf, "x"), parr, _ptr(dz, bf, "dz"), _ptr(dx, bf, "dx"), garr, S, dm,
+          int(n_heads), dff, int(n_hosts), int(causal), _stream(stream))
+
+
+def llama_stack_train_step(x, layer_params, dz, z, dx, layer_grads, n_heads, n_hosts, causal=True, stream=None):
+    """layer_params / layer_grads: one 9-element list per layer (as llama_layer_fwd / _bwd)."""
+    S, dm = (int(s) for s in x.shape)
+    dff = int(layer_params[0][6].shape[1])
+    bf = torch.bfloat16
+    keep_p, parr = _ptr_array([t for p in layer_params for t in p], bf, "params")
+    keep_g, garr = _ptr_array([t for g in layer_grads for t in g], torch.float32, "grads")
+    _call("llama_stack_train_step", _ptr(x, bf, "x"), parr, _ptr(dz, bf, "dz"), _ptr(z, bf, "z"), _ptr(dx, bf, "dx"),
+          garr, len(layer_params), S, dm, int(n_heads), dff, int(n_hosts), int(causal), _stream(stream))
 
 
 # ----------------------------------------------------------------------------------

@@ -30,6 +30,68 @@ int gemm(const GemmArgs& g, bool ta, bool tb, int epi, hipStream_t st) {
   return RA_OK;
 }
 
+// y (bf16) = x w (+ residual), row blocks of `block`
+int proj(const void* x, const void* w, const void* residual, void* y, int T, int din, int dout, int block,
+                hipStream_t st) {
+  for (int r0 = 0; r0 < T; r0 += block) {
+    GemmArgs g{};
+    g.A = (const char*)x + (size_t)r0 * din * 2;
+    g.B = w;
+    g.C = (char*)y + (size_t)r0 * dout * 2;
+    g.residual = residual ? (const char*)residual + (size_t)r0 * dout * 2 : nullptr;
+    g.lda = din;
+    g.ldb = dout;
+    g.ldc = dout;
+    g.M = block;
+    g.N = dout;
+    g.K = din;
+    int rc = gemm(g, false, false, EPI_BF16, st);
+    if (rc) return rc;
+  }
+  return RA_OK;
+}
+
+// dW (f32, overwritten) = x^T dy, accumulated over row blocks
+int wgrad(const void* x, const void* dy, float* dw, int T, int din, int dout, int block, hipStream_t st) {
+  for (int bi = 0, r0 = 0; r0 < T; ++bi, r0 += block) {
+    GemmArgs g{};
+    g.A = (const char*)x + (size_t)r0 * din * 2;
+    g.B = (const char*)dy + (size_t)r0 * dout * 2;
+    g.C = dw;
+    g.lda = din;
+    g.ldb = dout;
+    g.ldc = dout;
+    g.M = din;
+    g.N = dout;
+    g.K = block;
+    g.accumulate = bi > 0;
+    int rc = gemm(g, true, false, EPI_F32, st);
+    if (rc) return rc;
+  }
+  return RA_OK;
+}
+
+// dx32 (f32) (+)= dy w^T, row blocks
+int dgrad32(const void* dy, const void* w, float* dx32, int accumulate, int T, int din, int dout, int block,
+                   hipStream_t st) {
+  for (int r0 = 0; r0 < T; r0 += block) {
+    GemmArgs g{};
+    g.A = (const char*)dy + (size_t)r0 * dout * 2;
+    g.B = w;
+    g.C = dx32 + (size_t)r0 * din;
+    g.lda = dout;
+    g.ldb = dout;
+    g.ldc = din;
+    g.M = block;
+    g.N = din;
+    g.K = dout;
+    g.accumulate = accumulate;
+    int rc = gemm(g, false, true, EPI_F32, st);
+    if (rc) return rc;
+  }
+  return RA_OK;
+}
+
 int ffn_forward(const void* x, const void* w1, const void* b1, const void* w2, const void* b2, const void* residual,
                 void* y, int T, int d_model, int d_ff, int block, int act, hipStream_t stream) {
   int rc;

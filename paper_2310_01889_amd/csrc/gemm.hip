@@ -28,6 +28,9 @@ __device__ __forceinline__ float act_apply(float h) {
   return 0.5f * h * (1.f + erff(h * 0.7071067811865476f));
 }
 
+// silu(u) = u sigmoid(u) and its derivative sigmoid(u) (1 + u (1 - sigmoid(u))) (SwiGLU gate)
+__device__ __forceinline__ float sigmoid_f(float u) { return __builtin_amdgcn_rcpf(1.f + __expf(-u)); }
+
 template <int ACT>
 __device__ __forceinline__ float act_grad(float h) {
   constexpr int act = ACT;
@@ -200,6 +203,24 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] *= act_grad<ACT>(h[e]);
           *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        } else if (EPI == EPI_GLU_BF16) {
+          const f32x4 u = *(const f32x4*)(g.aux_f32 + off);
+          if (g.aux2_f32) *(f32x4*)(g.aux2_f32 + off) = f32x4{v[0], v[1], v[2], v[3]};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] *= u[e] * sigmoid_f(u[e]);
+          *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        } else if (EPI == EPI_GLU_GRAD) {
+          const f32x4 u = *(const f32x4*)(g.aux_f32 + off);
+          const f32x4 w = *(const f32x4*)(g.aux2_f32 + off);
+          float du[4], dw[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float sg = sigmoid_f(u[e]);
+            du[e] = v[e] * w[e] * sg * (1.f + u[e] * (1.f - sg));
+            dw[e] = v[e] * u[e] * sg;
+          }
+          *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(du[0], du[1]), pack_bf16x2(du[2], du[3])};
+          *(u32x2*)((bf16*)g.C2 + off) = u32x2{pack_bf16x2(dw[0], dw[1]), pack_bf16x2(dw[2], dw[3])};
         } else {  // EPI_F32: overwrite, or add into C
           f32x4* cp = (f32x4*)((float*)g.C + off);
           if (g.accumulate) {
@@ -267,6 +288,9 @@ hipError_t launch_gemm(const GemmArgs& g, bool ta, bool tb, int epi, hipStream_t
   RA_GEMM_CASE_ACT(false, true, EPI_ACT_GRAD_BF16)
   RA_GEMM_CASE(true, false, EPI_F32)
   RA_GEMM_CASE(false, true, EPI_F32)
+  RA_GEMM_CASE(false, false, EPI_F32)
+  RA_GEMM_CASE(false, false, EPI_GLU_BF16)
+  RA_GEMM_CASE(false, true, EPI_GLU_GRAD)
 #undef RA_GEMM_CASE
 #undef RA_GEMM_CASE_ACT
   return hipErrorInvalidValue;

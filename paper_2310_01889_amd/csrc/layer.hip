@@ -31,68 +31,6 @@ static int check_layer(int S, int dm, int H, int dff, int N, int causal, int act
   return RA_OK;
 }
 
-// y (bf16) = x w (+ residual), row blocks of `block`
-static int proj(const void* x, const void* w, const void* residual, void* y, int T, int din, int dout, int block,
-                hipStream_t st) {
-  for (int r0 = 0; r0 < T; r0 += block) {
-    GemmArgs g{};
-    g.A = (const char*)x + (size_t)r0 * din * 2;
-    g.B = w;
-    g.C = (char*)y + (size_t)r0 * dout * 2;
-    g.residual = residual ? (const char*)residual + (size_t)r0 * dout * 2 : nullptr;
-    g.lda = din;
-    g.ldb = dout;
-    g.ldc = dout;
-    g.M = block;
-    g.N = dout;
-    g.K = din;
-    int rc = gemm(g, false, false, EPI_BF16, st);
-    if (rc) return rc;
-  }
-  return RA_OK;
-}
-
-// dW (f32, overwritten) = x^T dy, accumulated over row blocks
-static int wgrad(const void* x, const void* dy, float* dw, int T, int din, int dout, int block, hipStream_t st) {
-  for (int bi = 0, r0 = 0; r0 < T; ++bi, r0 += block) {
-    GemmArgs g{};
-    g.A = (const char*)x + (size_t)r0 * din * 2;
-    g.B = (const char*)dy + (size_t)r0 * dout * 2;
-    g.C = dw;
-    g.lda = din;
-    g.ldb = dout;
-    g.ldc = dout;
-    g.M = din;
-    g.N = dout;
-    g.K = block;
-    g.accumulate = bi > 0;
-    int rc = gemm(g, true, false, EPI_F32, st);
-    if (rc) return rc;
-  }
-  return RA_OK;
-}
-
-// dx32 (f32) (+)= dy w^T, row blocks
-static int dgrad32(const void* dy, const void* w, float* dx32, int accumulate, int T, int din, int dout, int block,
-                   hipStream_t st) {
-  for (int r0 = 0; r0 < T; r0 += block) {
-    GemmArgs g{};
-    g.A = (const char*)dy + (size_t)r0 * dout * 2;
-    g.B = w;
-    g.C = dx32 + (size_t)r0 * din;
-    g.lda = dout;
-    g.ldb = dout;
-    g.ldc = din;
-    g.M = block;
-    g.N = din;
-    g.K = dout;
-    g.accumulate = accumulate;
-    int rc = gemm(g, false, true, EPI_F32, st);
-    if (rc) return rc;
-  }
-  return RA_OK;
-}
-
 // Forward activations shared by forward and backward: Q, K, V, O (bf16 [S, dm]), lse, Y.
 struct LayerActs {
   char *q, *k, *v, *o, *y;

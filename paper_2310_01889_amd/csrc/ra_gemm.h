@@ -11,7 +11,9 @@ enum GemmEpilogue {
   EPI_ACT_BF16 = 1,       // C = act(acc + bias[n]) (+ residual), stored bf16
   EPI_ACT_STORE_H = 2,    // aux_f32 = acc + bias (pre-activation, float32); C = act(aux_f32), bf16
   EPI_ACT_GRAD_BF16 = 3,  // C = acc * act'(aux_f32[m][n]), stored bf16
-  EPI_F32 = 4             // C = acc (or C += acc if accumulate), float32
+  EPI_F32 = 4,            // C = acc (or C += acc if accumulate), float32
+  EPI_GLU_BF16 = 5,       // C = silu(aux_f32[m][n]) * acc, bf16; aux2_f32 = acc if aux2_f32 != null
+  EPI_GLU_GRAD = 6        // with u = aux_f32, w = aux2_f32: C = acc * w * silu'(u), C2 = acc * silu(u) (bf16)
 };
 
 struct GemmArgs {
@@ -21,6 +23,8 @@ struct GemmArgs {
   const void* bias;       // bf16 [N] or null
   const void* residual;   // bf16 [M][ldc] or null
   float* aux_f32;         // float32 [M][ldc]: pre-activation (written or read)
+  float* aux2_f32;        // float32 [M][ldc]: second gate input of the GLU epilogues
+  void* C2;               // bf16 [M][ldc]: second output of EPI_GLU_GRAD
   long long lda, ldb, ldc;
   int M, N, K, act, accumulate;
 };

@@ -61,3 +61,22 @@ def layer_inputs(seed, S, d_model, d_ff, dtype=torch.bfloat16):
     w2 = _draw(g, (d_ff, d_model), dtype, 0.02)
     dz = _draw(g, (S, d_model), dtype)
     return x, wq, wk, wv, wo, w1, w2, dz
+
+
+def llama_layer_inputs(seed, S, d_model, d_ff, n_layers=1, dtype=torch.bfloat16):
+    """x [S,d_model]; per layer (g1 [d_model], Wq, Wk, Wv, Wo [d_model,d_model],
+    g2 [d_model], W1, W3 [d_model,d_ff], W2 [d_ff,d_model]); dZ [S,d_model]; drawn in that
+    order.  Gains are 1 + N(0, 0.1) (so that they matter), weights N(0, 0.02)."""
+    g = _gen(seed)
+    x = _draw(g, (S, d_model), dtype)
+    layers = []
+    for _ in range(n_layers):
+        g1 = (1.0 + 0.1 * torch.randn(d_model, generator=g)).to(dtype)
+        wq, wk, wv, wo = (_draw(g, (d_model, d_model), dtype, 0.02) for _ in range(4))
+        g2 = (1.0 + 0.1 * torch.randn(d_model, generator=g)).to(dtype)
+        w1 = _draw(g, (d_model, d_ff), dtype, 0.02)
+        w3 = _draw(g, (d_model, d_ff), dtype, 0.02)
+        w2 = _draw(g, (d_ff, d_model), dtype, 0.02)
+        layers.append([g1, wq, wk, wv, wo, g2, w1, w3, w2])
+    dz = _draw(g, (S, d_model), dtype)
+    return x, layers, dz

@@ -82,6 +82,30 @@ def test_decode_argument_validation(lib):
     assert dec(B=1 << 10, H=64, S=1 << 16, N=8) == RA_EUNSUPPORTED
 
 
+def test_llama_argument_validation(lib):
+    P9 = (ctypes.c_void_p * 9)(*([0x1000] * 9))
+    pp = ctypes.cast(P9, ctypes.c_void_p)
+    f = lib.llama_layer_fwd
+    assert f(NULL, pp, FAKE, 1024, 256, 2, 512, 4, 1, NULL) == RA_EINVAL
+    assert f(FAKE, pp, FAKE, 1024, 256, 3, 512, 4, 1, NULL) == RA_EUNSUPPORTED   # d_model % n_heads
+    assert f(FAKE, pp, FAKE, 1024, 384, 4, 512, 4, 1, NULL) == RA_EUNSUPPORTED   # head dim 96
+    assert f(FAKE, pp, FAKE, 1024, 256, 2, 500, 4, 1, NULL) == RA_EUNSUPPORTED   # d_ff % 256
+    assert f(FAKE, pp, FAKE, 1024, 256, 2, 512, 8, 1, NULL) == RA_EUNSUPPORTED   # block 128 < 256
+    assert f(FAKE, pp, FAKE, 1024, 16384, 128, 512, 4, 1, NULL) == RA_EUNSUPPORTED  # d_model > 8192
+    bad = (ctypes.c_void_p * 9)(*([0x1000] * 8 + [0]))
+    assert f(FAKE, ctypes.cast(bad, ctypes.c_void_p), FAKE, 1024, 256, 2, 512, 4, 1, NULL) == RA_EINVAL
+    assert lib.llama_stack_train_step(FAKE, pp, FAKE, FAKE, FAKE, pp, 0, 1024, 256, 2, 512, 4, 1, NULL) == RA_EINVAL
+    assert lib.rms_norm_fwd(FAKE, FAKE, FAKE, NULL, 16, 12, NULL) == RA_EUNSUPPORTED  # d % 8
+    assert lib.rms_norm_fwd(FAKE, FAKE, FAKE, NULL, 16, 16384, NULL) == RA_EUNSUPPORTED
+    assert lib.rms_norm_bwd(FAKE, FAKE, FAKE, NULL, FAKE, NULL, 16, 256, NULL) == RA_EINVAL
+    assert lib.rope_apply(FAKE, 16, 2, 6, 0, 0, NULL) == RA_EUNSUPPORTED  # D % 4
+    assert lib.rope_apply(FAKE, 16, 2, 8, -1, 0, NULL) == RA_EINVAL
+    assert lib.rope_apply(FAKE, 16, 2, 8, 0, 2, NULL) == RA_EINVAL
+    assert lib.swiglu_ffn(FAKE, FAKE, FAKE, FAKE, NULL, FAKE, 512, 256, 300, 256, NULL) == RA_EUNSUPPORTED
+    assert lib.swiglu_ffn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NULL, FAKE, 512, 256, 512, 256,
+                              NULL) == RA_EINVAL
+
+
 def test_ffn_argument_validation(lib):
     f = lib.blockwise_ffn
     assert f(FAKE, FAKE, NULL, FAKE, NULL, FAKE, 512, 256, 512, 256, 5, NULL) == RA_EINVAL
