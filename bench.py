@@ -16,7 +16,8 @@ launch, on the stream it runs on) against the bf16 dense matrix-core peak.  The
 `cpu_baseline` object times the fp64 CPU oracle on one head of the same workload and
 scales it to all 32 heads.  `extra` holds secondary configurations measured in the same
 run (forward+backward at S=16384, one host's share at 262144 tokens, ring decode of 1 and 8
-tokens against a 262144-token cache, blockwise FFN and the full layer) for context.
+tokens against a 262144-token cache, blockwise FFN, the Algorithm 1 layer and a 2-layer
+LLaMA-style training step) for context.
 """
 import argparse
 import json
@@ -231,6 +232,23 @@ def main():
         extra["layer_fwd_bwd_S65536_d4096"] = {"ms": round(msl, 3), "tflops": round(flayer / msl / 1e9, 2),
                                                "tokens_per_s": round(S4 / (msl * 1e-3), 1),
                                                "note": "algorithmic flops; backward recomputes the forward"}
+        del x4, dz4, wq, wk, wv, wo, w1, w2, y4, z4, dx4, dws
+        # training step of a 2-layer LLaMA-7B-width stack (RMSNorm, RoPE, SwiGLU d_ff 11008,
+        # pre-norm) around ring attention, S = 65536 in 8 host blocks, full recomputation
+        nl, dffl = 2, 11008
+        xl, dzl = mk(S4, dm), mk(S4, dm)
+        gain = lambda: (1.0 + 0.1 * torch.randn(dm, generator=g, device="cuda")).to(torch.bfloat16)
+        params = [[gain(), w(dm, dm), w(dm, dm), w(dm, dm), w(dm, dm), gain(), w(dm, dffl), w(dm, dffl), w(dffl, dm)]
+                  for _ in range(nl)]
+        grads = [[torch.empty(t.shape, dtype=torch.float32, device="cuda") for t in p] for p in params]
+        zl, dxl = torch.empty_like(xl), torch.empty_like(xl)
+        msll, _ = time_calls(lambda: ra.llama_stack_train_step(xl, params, dzl, zl, dxl, grads, H4, N4), 2, 1)
+        gemm_fwd = 2.0 * S4 * (4 * dm * dm + 3 * dm * dffl)
+        fll = nl * (3 * gemm_fwd + 3.5 * fatt)
+        extra["llama_stack2_train_step_S65536_d4096_ff11008"] = {
+            "ms": round(msll, 2), "tflops": round(fll / msll / 1e9, 2), "tokens_per_s": round(S4 / (msll * 1e-3), 1),
+            "note": "algorithmic flops (GEMMs fwd + 2x bwd, attention fwd + 2.5x bwd); the backward recomputes "
+                    "each layer's forward"}
         out["extra"] = extra
 
     if not args.no_cpu:

@@ -55,3 +55,71 @@ def layer_rounding_errors(x, wq, wk, wv, wo, w1, w2, dz, n_heads):
         out[name + "_scaled_max"] = float(((got - ref).abs() / ref.abs().clamp(min=1.0)).max())
         out[name + "_rel_rms"] = float((got - ref).pow(2).mean().sqrt() / ref.pow(2).mean().sqrt())
     return out
+
+
+def llama_layer_rounding_errors(x, params, dz, n_heads):
+    """The LLaMA-style layer (oracle/llama.py) in exact arithmetic except for bf16 storage
+    where the GPU path stores bf16: n1, q, k, v, the rotated q and k, P, the attention
+    output, h, n2, the gate output, z; backward dh, dO, P, dS, the rotated-q/k gradients and
+    dv, dq and dk after the inverse rotation, du, dw, dx (x W1, x W3 and the normalisation
+    gradients stay float32, as there).  Returns, for z, dx and every parameter gradient,
+    (max |err|, rms of the exact value, relative RMS error) against the fp64 oracle."""
+    from oracle import llama as LL
+
+    S, dm = x.shape
+    H, D = n_heads, dm // n_heads
+    X, dZ = x.double(), dz.double()
+    g1, Wq, Wk, Wv, Wo, g2, W1, W3, W2 = (t.double() for t in params)
+    pos = np.arange(S)
+    rot = lambda t, inv=False: torch.from_numpy(LL.rope(t.view(S, H, D).numpy(), pos, inverse=inv)).reshape(S, dm)
+    norm = lambda t, g: t / torch.sqrt((t * t).mean(1, keepdim=True) + LL.EPS) * g
+    mask = torch.ones(S, S, dtype=torch.bool).triu(1)
+    heads = lambda t: t.view(S, H, D).transpose(0, 1)
+    flat = lambda t: t.transpose(0, 1).reshape(S, dm)
+    n1 = _bf(norm(X, g1))
+    q, k, v = (_bf(n1 @ W) for W in (Wq, Wk, Wv))
+    qr, kr = _bf(rot(q)), _bf(rot(k))
+    Q, K, V = heads(qr), heads(kr), heads(v)
+    s = (Q @ K.transpose(1, 2) / math.sqrt(D)).masked_fill(mask, float("-inf"))
+    P = torch.softmax(s, dim=-1)
+    Pb = _bf(torch.exp(s - s.max(-1, keepdim=True).values))
+    A = _bf((Pb @ V) / Pb.sum(-1, keepdim=True))
+    a = flat(A)
+    h = _bf(X + a @ Wo)
+    n2 = _bf(norm(h, g2))
+    u, w = n2 @ W1, n2 @ W3
+    sig = torch.sigmoid(u)
+    gte = _bf(u * sig * w)
+    Z = _bf(h + gte @ W2)
+    dgte = dZ @ W2.T
+    du, dw = _bf(dgte * w * sig * (1 + u * (1 - sig))), _bf(dgte * u * sig)
+    dW2, dW1, dW3 = gte.T @ dZ, n2.T @ du, n2.T @ dw
+    dn2 = du @ W1.T + dw @ W3.T
+    dh_n, dG2 = LL.rmsnorm_bwd(h.numpy(), g2.numpy(), dn2.numpy())
+    dh = _bf(dZ + torch.from_numpy(dh_n))
+    dWo = a.T @ dh
+    dO = heads(_bf(dh @ Wo.T))
+    delta = (dO * A).sum(-1, keepdim=True)
+    dS = _bf(P * (dO @ V.transpose(1, 2) - delta))
+    dqr = _bf(flat(dS @ K / math.sqrt(D)))
+    dkr = _bf(flat(dS.transpose(1, 2) @ Q / math.sqrt(D)))
+    dv = _bf(flat(_bf(P).transpose(1, 2) @ dO))
+    dq, dk = _bf(rot(dqr, True)), _bf(rot(dkr, True))
+    dWq, dWk, dWv = n1.T @ dq, n1.T @ dk, n1.T @ dv
+    dn1 = dq @ Wq.T + dk @ Wk.T + dv @ Wv.T
+    dx_n, dG1 = LL.rmsnorm_bwd(X.numpy(), g1.numpy(), dn1.numpy())
+    dX = _bf(dh + torch.from_numpy(dx_n))
+    p64 = [t.float().numpy() for t in params]
+    z_ref = LL.layer_fwd(x.float().numpy(), *p64, H)
+    ref = LL.layer_bwd(x.float().numpy(), *p64, dz.float().numpy(), H)
+    got = [Z, dX, torch.from_numpy(dG1), dWq, dWk, dWv, dWo, torch.from_numpy(dG2), dW1, dW3, dW2]
+    names = ["z", "dx", "g1", "wq", "wk", "wv", "wo", "g2", "w1", "w3", "w2"]
+    out = {}
+    for name, g_, r in zip(names, got, [z_ref] + list(ref)):
+        g_ = g_.numpy() if torch.is_tensor(g_) else g_
+        err = np.abs(g_ - r)
+        rms = float(np.sqrt(np.mean(r * r)))
+        out[name] = (float(err.max()), rms, float(np.sqrt(np.mean(err * err))) / max(rms, 1e-30))
+        if name in ("z", "dx"):  # magnitude-scaled max, the metric of the z / dx bounds
+            out[name + "_scaled_max"] = float((err / np.maximum(1.0, np.abs(r))).max())
+    return out
