@@ -68,36 +68,48 @@ __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const 
 }
 
 // =====================================================================================
-// bf16 dK/dV kernel: 4 waves x 32 keys = 128 keys per workgroup; loops over 64-query
+// bf16 dK/dV kernel: 4 waves x 32 keys = 128 keys per workgroup; loops over 32-query
 // tiles of the host's block.  Per wave, lanes run over the wave's keys:
-//   S  = Q K^T            [query x key] (A = Q rows from LDS with row bits 2 and 3
-//                          swapped, B = K of the wave's keys held in registers)
-//   P  = exp2(S log2e/sqrt(D) - lse log2e)                       (masked -> 0)
+//   S' = Q (K log2e/sqrt(D))^T - lse log2e   [query x key] (A = Q rows from LDS with
+//        row bits 2 and 3 swapped, B = the pre-scaled K of the wave's keys in registers;
+//        the accumulator starts at -lse log2e of its query, so S' comes out ready)
+//   P  = exp2(S')                                               (masked -> 0)
 //   dP = dO V^T - Delta   (A = dO rows, B = V in registers; starts at -Delta)
 //   dS = P * dP
 //   dV^T += dO^T P        (A = dO^T by LDS transpose read, B = P)
 //   dK^T += Q^T dS        (A = Q^T by LDS transpose read, B = dS)
 // Q and dO tiles (XOR-swizzled rows) and the tile's lse*log2e and Delta are filled by
-// direct-to-LDS buffer loads, double buffered.
+// direct-to-LDS buffer loads into a ring of three buffers (48 KB for D = 128, so every
+// LDS address fits the reads' immediate offsets).  The loop is software pipelined: while
+// tile t's P and dS are formed on the vector ALUs and its dV, dK products run, the S' and
+// dP products of tile t+1 are issued and tile t+2 streams in.
 // =====================================================================================
-constexpr int kKB = 128, kQB = 64, kBT = 256;
+constexpr int kKB = 128, kQB = 32, kBT = 256;
 
 template <int D>
 __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) {
   constexpr int NKK = D / 16, NDT = D / 32, CPR = D / 8;
   constexpr int ROWS_PER_LOAD = 64 / CPR, LOADS = kQB / 4 / ROWS_PER_LOAD;
-  // one LDS object per buffer, so that reads of one buffer are known not to alias the
-  // direct-to-LDS loads in flight into the other (else the compiler waits for them)
+  static_assert(LOADS >= 1, "each wave fills at least one 1 KB row group");
+  // one LDS object per buffer, so that reads of one are known not to alias the
+  // direct-to-LDS loads in flight into another (else the compiler waits for them)
   __shared__ __attribute__((aligned(1024))) bf16 sQ0[kQB * D];
   __shared__ __attribute__((aligned(1024))) bf16 sQ1[kQB * D];
-  __shared__ __attribute__((aligned(1024))) bf16 sO0[kQB * D];  // dO tile
+  __shared__ __attribute__((aligned(1024))) bf16 sQ2[kQB * D];
+  __shared__ __attribute__((aligned(1024))) bf16 sO0[kQB * D];  // dO tiles
   __shared__ __attribute__((aligned(1024))) bf16 sO1[kQB * D];
-  __shared__ __attribute__((aligned(256))) float sL0[kQB];       // lse * log2e
-  __shared__ __attribute__((aligned(256))) float sL1[kQB];
-  __shared__ __attribute__((aligned(256))) float sD0[kQB];       // Delta
-  __shared__ __attribute__((aligned(256))) float sD1[kQB];
-  auto pick = [](auto Bc, auto* a, auto* b) __attribute__((always_inline)) {
-    if constexpr (decltype(Bc)::value == 0) return a; else return b;
+  __shared__ __attribute__((aligned(1024))) bf16 sO2[kQB * D];
+  // lse * log2e and Delta: 64 floats each, as a one-wave 4-byte load writes 256 bytes
+  // (lanes past the tile read zero)
+  __shared__ __attribute__((aligned(256))) float sL0[64];
+  __shared__ __attribute__((aligned(256))) float sL1[64];
+  __shared__ __attribute__((aligned(256))) float sL2[64];
+  __shared__ __attribute__((aligned(256))) float sD0[64];
+  __shared__ __attribute__((aligned(256))) float sD1[64];
+  __shared__ __attribute__((aligned(256))) float sD2[64];
+  auto pick = [](auto Bc, auto* a, auto* b, auto* c) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value % 3;
+    if constexpr (B == 0) return a; else if constexpr (B == 1) return b; else return c;
   };
 
   const int n_kt = p.c / kKB;
@@ -110,6 +122,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   const StepHost hs = p.host[slot];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int rs = p.H * D;
+  const float sl2 = p.scale * kLog2e;
 
   const int key_in_blk = kt * kKB + wave * 32 + l32;  // this lane's key (B-operand column)
   const int kpos = hs.k_pos0 + key_in_blk;
@@ -118,7 +131,9 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   bf16x8 kreg[NKK], vreg[NKK];
 #pragma unroll
   for (int kk = 0; kk < NKK; ++kk) {
-    kreg[kk] = *(const bf16x8*)(krow + 16 * kk + 8 * hi);
+    const bf16x8 kx = *(const bf16x8*)(krow + 16 * kk + 8 * hi);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kreg[kk][e] = (bf16)((float)kx[e] * sl2);  // scores in log2 units
     vreg[kk] = *(const bf16x8*)(vrow + 16 * kk + 8 * hi);
   }
   f32x16 dkacc[NDT], dvacc[NDT];
@@ -143,21 +158,24 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   const bf16* qbase = (const bf16*)p.q + (long long)b * p.q_bstride + h * D;
   const bf16* obase = (const bf16*)p.dO + (long long)b * p.q_bstride + h * D;
   const long long lrow0 = (long long)bh * p.Sq + hs.q_row0;
+  constexpr int RPW = kQB / 4;  // tile rows each wave fills
   int goff[LOADS];
 #pragma unroll
   for (int j = 0; j < LOADS; ++j) {
-    const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
+    const int r = wave * RPW + j * ROWS_PER_LOAD + lane / CPR;
     goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
   }
   auto load_tile = [&](int qt, auto Bc) __attribute__((always_inline)) {
     const long long t0 = (long long)(hs.q_row0 + qt * kQB) * rs;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      buffer_load_lds16(qbase + t0, kQB * rs * 2, pick(Bc, sQ0, sQ1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
-      buffer_load_lds16(obase + t0, kQB * rs * 2, pick(Bc, sO0, sO1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16(qbase + t0, kQB * rs * 2, pick(Bc, sQ0, sQ1, sQ2) + (wave * RPW + j * ROWS_PER_LOAD) * D,
+                        goff[j]);
+      buffer_load_lds16(obase + t0, kQB * rs * 2, pick(Bc, sO0, sO1, sO2) + (wave * RPW + j * ROWS_PER_LOAD) * D,
+                        goff[j]);
     }
-    if (wave == 0) buffer_load_lds4(p.lse + lrow0 + qt * kQB, kQB * 4, pick(Bc, sL0, sL1), 4 * lane);
-    if (wave == 1) buffer_load_lds4(p.delta + lrow0 + qt * kQB, kQB * 4, pick(Bc, sD0, sD1), 4 * lane);
+    if (wave == 0) buffer_load_lds4(p.lse + lrow0 + qt * kQB, kQB * 4, pick(Bc, sL0, sL1, sL2), 4 * lane);
+    if (wave == 1) buffer_load_lds4(p.delta + lrow0 + qt * kQB, kQB * 4, pick(Bc, sD0, sD1, sD2), 4 * lane);
   };
   const int qrow = swap_bits23(l32);
   int roff[NKK];
@@ -173,94 +191,187 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       const int d = 32 * dt + 16 * (g16 & 1) + 4 * (li & 3);
       toff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
-  const float sl2 = p.scale * kLog2e;
 
-  auto body = [&](auto Bc, auto Mc, int qt) __attribute__((always_inline)) {
-    constexpr int B = decltype(Bc)::value;
+  // accumulator starts of S' (-lse log2e) and dP (-Delta) of a tile: register 8 g + e of a
+  // lane holds query 16 g + 8 hi + e
+  auto inits = [&](auto Bc, f32x16& si, f32x16& di) __attribute__((always_inline)) {
+    const float* sl = pick(Bc, sL0, sL1, sL2);
+    const float* sd = pick(Bc, sD0, sD1, sD2);
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const int q0 = 16 * g + 8 * hi;
+      const f32x4 la = *(const f32x4*)&sl[q0], lb = *(const f32x4*)&sl[q0 + 4];
+      const f32x4 da = *(const f32x4*)&sd[q0], db = *(const f32x4*)&sd[q0 + 4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        si[8 * g + e] = -la[e];
+        si[8 * g + 4 + e] = -lb[e];
+        di[8 * g + e] = -da[e];
+        di[8 * g + 4 + e] = -db[e];
+      }
+    }
+  };
+  // P and dS (bf16 pairs) of group g (16 queries) of a tile, pair u of the group's 4
+  auto unit = [&](auto Mc, const f32x16& sc, const f32x16& dpc, int qpos0, int g, int u, uint32_t& w1,
+                  uint32_t& w2) __attribute__((always_inline)) {
     constexpr bool MASK = decltype(Mc)::value;
-    if (qt + 1 < n_qtiles) load_tile(qt + 1, std::integral_constant<int, B ^ 1>{});
-    const bf16* qtl = pick(Bc, sQ0, sQ1);
-    const bf16* otl = pick(Bc, sO0, sO1);
-    const float* sDb = pick(Bc, sD0, sD1);
-    const float* sLb = pick(Bc, sL0, sL1);
+    float pv[2], dsv[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int r = 8 * g + 2 * u + e;
+      float pr = fast_exp2(sc[r]);
+      if (MASK && kpos > qpos0 + 16 * g + 8 * hi + 2 * u + e) pr = 0.f;
+      pv[e] = pr;
+      dsv[e] = pr * dpc[r];
+    }
+    w1 = pack_bf16x2(pv[0], pv[1]);
+    w2 = pack_bf16x2(dsv[0], dsv[1]);
+  };
+
+  // One tile t (buffer Bc): loads of tile t+2 (buffer Bc+2), the S'/dP products of tile t+1
+  // (buffer Bc+1; Nc: it exists) and, for tile t, P and dS in two groups of 16 queries, each
+  // followed by its dV and dK products; then the wait for tile t+2 and the barrier that frees
+  // buffer Bc.  For D = 128 the region is laid out by hand in 20 fenced steps: step s issues
+  // S'/dP product s (s < 16; S' and dP alternate, so consecutive products are independent),
+  // the dV/dK product s - 4 (s >= 4; group (s - 4) / 8) and the vector work of one pair unit
+  // (group 0 at steps 0..3, group 1 at steps 4, 6, 8, 10), with LDS operand reads two steps
+  // ahead.  Other head dims run the same work in program order.
+  auto tile = [&](auto Bc, auto Mc, auto Nc, int qt, f32x16& s_cur, f32x16& dp_cur) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value;
+    constexpr bool NX = decltype(Nc)::value;
+    using Bn = std::integral_constant<int, (B + 1) % 3>;
+    using Bl = std::integral_constant<int, (B + 2) % 3>;
+    if (qt + 2 < n_qtiles) load_tile(qt + 2, Bl{});
+    const bf16* qn = pick(Bn{}, sQ0, sQ1, sQ2);  // next tile: row reads
+    const bf16* on = pick(Bn{}, sO0, sO1, sO2);
+    const bf16* qc = pick(Bc, sQ0, sQ1, sQ2);    // this tile: transpose reads
+    const bf16* oc = pick(Bc, sO0, sO1, sO2);
     const int qpos0 = hs.q_pos0 + qt * kQB;
-    // S and dP (rows = queries 32 qm + 16 (i/8) + 8 hi + i%8 of the tile)
-    f32x16 sacc[2], dpacc[2];
+    f32x16 s_nx, dp_nx;
+    if constexpr (NX) inits(Bn{}, s_nx, dp_nx);
+    if constexpr (D == 128) {
+      bf16x8 aop[16], top[16];
+      uint32_t wp[2][4], ws[2][4];
+      bf16x8 pb[2], dsb[2];
+      constexpr int kPF = 2;
+      auto read_a = [&](auto Sc) __attribute__((always_inline)) {  // product s: kk = s / 2, dP if odd
+        constexpr int S = decltype(Sc)::value;
+        aop[S] = *(const bf16x8*)(((S & 1) ? on : qn) + roff[S / 2]);
+      };
+      auto read_t = [&](auto Qc) __attribute__((always_inline)) {  // product q: group q / 8, dt (q % 8) / 2
+        constexpr int Q = decltype(Qc)::value, g = Q / 8, dt = (Q % 8) / 2;
+        const bf16* src = (Q & 1) ? qc : oc;
+        const bf16x4 lo = lds_read_tr16(src + 16 * g * D + toff[0][dt]);
+        const bf16x4 up = lds_read_tr16(src + 16 * g * D + toff[1][dt]);
+        top[Q] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+      };
+      if constexpr (NX) static_for<0, kPF>([&](auto Sc) __attribute__((always_inline)) { read_a(Sc); });
+      static_for<0, 20>([&](auto Sc) __attribute__((always_inline)) {
+        constexpr int S = decltype(Sc)::value;
+        if constexpr (NX && S + kPF < 16) read_a(std::integral_constant<int, S + kPF>{});
+        if constexpr (S + kPF >= 4 && S + kPF < 20) read_t(std::integral_constant<int, S + kPF - 4>{});
+        if constexpr (NX && S < 16) {
+          if constexpr (S & 1)
+            dp_nx = mfma32(aop[S], vreg[S / 2], dp_nx);
+          else
+            s_nx = mfma32(aop[S], kreg[S / 2], s_nx);
+        }
+        if constexpr (S >= 4) {
+          constexpr int q = S - 4, g = q / 8, dt = (q % 8) / 2;
+          if constexpr (q % 8 == 0) {
+            pb[g] = __builtin_bit_cast(bf16x8, u32x4{wp[g][0], wp[g][1], wp[g][2], wp[g][3]});
+            dsb[g] = __builtin_bit_cast(bf16x8, u32x4{ws[g][0], ws[g][1], ws[g][2], ws[g][3]});
+          }
+          if constexpr (q & 1)
+            dkacc[dt] = mfma32(top[q], dsb[g], dkacc[dt]);
+          else
+            dvacc[dt] = mfma32(top[q], pb[g], dvacc[dt]);
+        }
+        if constexpr (S < 4) {
+          unit(Mc, s_cur, dp_cur, qpos0, 0, S, wp[0][S], ws[0][S]);
+        } else if constexpr (S < 12 && S % 2 == 0) {
+          unit(Mc, s_cur, dp_cur, qpos0, 1, (S - 4) / 2, wp[1][(S - 4) / 2], ws[1][(S - 4) / 2]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    } else {
+      if constexpr (NX) {
 #pragma unroll
-    for (int qm = 0; qm < 2; ++qm) {
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        const int q0 = 32 * qm + 16 * hb + 8 * hi;
-        const f32x4 da = *(const f32x4*)&sDb[q0];
-        const f32x4 db = *(const f32x4*)&sDb[q0 + 4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          dpacc[qm][8 * hb + e] = -da[e];
-          dpacc[qm][8 * hb + 4 + e] = -db[e];
-          sacc[qm][8 * hb + e] = 0.f;
-          sacc[qm][8 * hb + 4 + e] = 0.f;
+        for (int kk = 0; kk < NKK; ++kk) {
+          s_nx = mfma32(*(const bf16x8*)(qn + roff[kk]), kreg[kk], s_nx);
+          dp_nx = mfma32(*(const bf16x8*)(on + roff[kk]), vreg[kk], dp_nx);
         }
       }
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
-        sacc[qm] = mfma32(*(const bf16x8*)(qtl + 32 * qm * D + roff[kk]), kreg[kk], sacc[qm]);
-        dpacc[qm] = mfma32(*(const bf16x8*)(otl + 32 * qm * D + roff[kk]), vreg[kk], dpacc[qm]);
-      }
-    }
-    // P, dS (bf16) and the two transposed products, 16 queries at a time
+      for (int g = 0; g < 2; ++g) {
+        uint32_t wp[4], ws[4];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const int qm = kb >> 1, hb = kb & 1;
-      const int q0 = 32 * qm + 16 * hb + 8 * hi;
-      const f32x4 la = *(const f32x4*)&sLb[q0];
-      const f32x4 lb = *(const f32x4*)&sLb[q0 + 4];
-      u32x4 wp, ws;
+        for (int u = 0; u < 4; ++u) unit(Mc, s_cur, dp_cur, qpos0, g, u, wp[u], ws[u]);
+        const bf16x8 pbg = __builtin_bit_cast(bf16x8, u32x4{wp[0], wp[1], wp[2], wp[3]});
+        const bf16x8 dsg = __builtin_bit_cast(bf16x8, u32x4{ws[0], ws[1], ws[2], ws[3]});
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float pv[2], dsv[2];
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int ee = 2 * j + e;
-          const float lv = ee < 4 ? la[ee] : lb[ee - 4];
-          float pr = fast_exp2(fmaf(sacc[qm][8 * hb + ee], sl2, -lv));
-          if (MASK && kpos > qpos0 + q0 + ee) pr = 0.f;
-          pv[e] = pr;
-          dsv[e] = pr * dpacc[qm][8 * hb + ee];
+        for (int dt = 0; dt < NDT; ++dt) {
+          const bf16x4 olo = lds_read_tr16(oc + 16 * g * D + toff[0][dt]);
+          const bf16x4 oup = lds_read_tr16(oc + 16 * g * D + toff[1][dt]);
+          dvacc[dt] = mfma32(bf16x8{olo[0], olo[1], olo[2], olo[3], oup[0], oup[1], oup[2], oup[3]}, pbg, dvacc[dt]);
+          const bf16x4 qlo = lds_read_tr16(qc + 16 * g * D + toff[0][dt]);
+          const bf16x4 qup = lds_read_tr16(qc + 16 * g * D + toff[1][dt]);
+          dkacc[dt] = mfma32(bf16x8{qlo[0], qlo[1], qlo[2], qlo[3], qup[0], qup[1], qup[2], qup[3]}, dsg, dkacc[dt]);
         }
-        wp[j] = pack_bf16x2(pv[0], pv[1]);
-        ws[j] = pack_bf16x2(dsv[0], dsv[1]);
-      }
-      const bf16x8 pb = __builtin_bit_cast(bf16x8, wp);
-      const bf16x8 dsb = __builtin_bit_cast(bf16x8, ws);
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x4 olo = lds_read_tr16(otl + 16 * kb * D + toff[0][dt]);
-        const bf16x4 oup = lds_read_tr16(otl + 16 * kb * D + toff[1][dt]);
-        dvacc[dt] = mfma32(bf16x8{olo[0], olo[1], olo[2], olo[3], oup[0], oup[1], oup[2], oup[3]}, pb, dvacc[dt]);
-        const bf16x4 qlo = lds_read_tr16(qtl + 16 * kb * D + toff[0][dt]);
-        const bf16x4 qup = lds_read_tr16(qtl + 16 * kb * D + toff[1][dt]);
-        dkacc[dt] = mfma32(bf16x8{qlo[0], qlo[1], qlo[2], qlo[3], qup[0], qup[1], qup[2], qup[3]}, dsb, dkacc[dt]);
       }
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tile t+2 landed
+    __syncthreads();                                   // and buffer Bc is free again
+    if constexpr (NX) {
+      s_cur = s_nx;
+      dp_cur = dp_nx;
+    }
+  };
+
+  if (qt0 < n_qtiles) {
+    load_tile(qt0, std::integral_constant<int, 0>{});
+    if (qt0 + 1 < n_qtiles) load_tile(qt0 + 1, std::integral_constant<int, 1>{});
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-  };
-  auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
-    int it = a;
-    if (((it - qt0) & 1) && it < e) body(std::integral_constant<int, 1>{}, Mc, it++);
-    for (; it + 1 < e; it += 2) {
-      body(std::integral_constant<int, 0>{}, Mc, it);
-      body(std::integral_constant<int, 1>{}, Mc, it + 1);
+    f32x16 s_cur, dp_cur;  // S' and dP of the tile being processed
+    inits(std::integral_constant<int, 0>{}, s_cur, dp_cur);
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      s_cur = mfma32(*(const bf16x8*)(sQ0 + roff[kk]), kreg[kk], s_cur);
+      dp_cur = mfma32(*(const bf16x8*)(sO0 + roff[kk]), vreg[kk], dp_cur);
     }
-    if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
-  };
-  if (qt0 < n_qtiles) load_tile(qt0, std::integral_constant<int, 0>{});
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  run(std::true_type{}, qt0, qt_free);
-  run(std::false_type{}, qt_free, n_qtiles);
+    // buffer of tile qt is (qt - qt0) % 3, known at compile time in a loop unrolled by 3;
+    // tiles [a, e) all have a successor
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
+      int it = a;
+      if (it < e && (it - qt0) % 3 == 1) tile(I1{}, Mc, std::true_type{}, it++, s_cur, dp_cur);
+      if (it < e && (it - qt0) % 3 == 2) tile(I2{}, Mc, std::true_type{}, it++, s_cur, dp_cur);
+      for (; it + 2 < e; it += 3) {
+        tile(I0{}, Mc, std::true_type{}, it, s_cur, dp_cur);
+        tile(I1{}, Mc, std::true_type{}, it + 1, s_cur, dp_cur);
+        tile(I2{}, Mc, std::true_type{}, it + 2, s_cur, dp_cur);
+      }
+      if (it < e) tile(I0{}, Mc, std::true_type{}, it++, s_cur, dp_cur);
+      if (it < e) tile(I1{}, Mc, std::true_type{}, it++, s_cur, dp_cur);
+    };
+    const int ql = n_qtiles - 1;
+    const int split = max(qt0, min(qt_free, ql));  // masked tiles first
+    run(std::true_type{}, qt0, split);
+    run(std::false_type{}, split, ql);
+    // last tile: no successor
+    const int ph = (ql - qt0) % 3;
+    auto last = [&](auto Mc) __attribute__((always_inline)) {
+      if (ph == 0) tile(I0{}, Mc, std::false_type{}, ql, s_cur, dp_cur);
+      else if (ph == 1) tile(I1{}, Mc, std::false_type{}, ql, s_cur, dp_cur);
+      else tile(I2{}, Mc, std::false_type{}, ql, s_cur, dp_cur);
+    };
+    if (ql < qt_free) last(std::true_type{}); else last(std::false_type{});
+  }
 
-  // add into the float32 gradient of the block (its home rows)
+  // add into the float32 gradient of the block (its home rows); dK carries the 1/sqrt(D)
   const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key_in_blk) * rs + h * D;
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
