@@ -18,10 +18,11 @@ namespace {
 
 // -------------------------------------------------------------------------------------
 // Delta_r = sum_d dO_rd * O_rd  (float32 [B, H, S]); rows in memory order (b, r, h).
+// The bf16 step kernels take -Delta and -lse log2e (their accumulators start there).
 // -------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const bf16* dO, const float* lse,
-                                                           float* delta, float* lse2, int B, int S, int H) {
+                                                           float* ndelta, float* nlse2, int B, int S, int H) {
   constexpr int TPR = D / 8;  // threads per row
   const long long row = (long long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
   const int c = (threadIdx.x % TPR) * 8;
@@ -39,8 +40,8 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const 
     const long long br = row / H;
     const int r = (int)(br % S), b = (int)(br / S);
     const long long idx = ((long long)b * H + h) * S + r;
-    delta[idx] = s;
-    lse2[idx] = lse[idx] * kLog2e;  // the bf16 step kernels work in log2 units
+    ndelta[idx] = -s;
+    nlse2[idx] = -lse[idx] * kLog2e;  // the bf16 step kernels work in log2 units
   }
 }
 
@@ -101,10 +102,10 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   __shared__ __attribute__((aligned(1024))) bf16 sO2[kQB * D];
   // lse * log2e and Delta: 64 floats each, as a one-wave 4-byte load writes 256 bytes
   // (lanes past the tile read zero)
-  __shared__ __attribute__((aligned(256))) float sL0[64];
+  __shared__ __attribute__((aligned(256))) float sL0[64];  // -lse log2e
   __shared__ __attribute__((aligned(256))) float sL1[64];
   __shared__ __attribute__((aligned(256))) float sL2[64];
-  __shared__ __attribute__((aligned(256))) float sD0[64];
+  __shared__ __attribute__((aligned(256))) float sD0[64];  // -Delta
   __shared__ __attribute__((aligned(256))) float sD1[64];
   __shared__ __attribute__((aligned(256))) float sD2[64];
   auto pick = [](auto Bc, auto* a, auto* b, auto* c) __attribute__((always_inline)) {
@@ -192,8 +193,8 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       toff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
 
-  // accumulator starts of S' (-lse log2e) and dP (-Delta) of a tile: register 8 g + e of a
-  // lane holds query 16 g + 8 hi + e
+  // accumulator starts of S' (-lse log2e) and dP (-Delta), stored negated by the
+  // preprocess kernel, of a tile: register 8 g + e of a lane holds query 16 g + 8 hi + e
   auto inits = [&](auto Bc, f32x16& si, f32x16& di) __attribute__((always_inline)) {
     const float* sl = pick(Bc, sL0, sL1, sL2);
     const float* sd = pick(Bc, sD0, sD1, sD2);
@@ -204,10 +205,10 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       const f32x4 da = *(const f32x4*)&sd[q0], db = *(const f32x4*)&sd[q0 + 4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        si[8 * g + e] = -la[e];
-        si[8 * g + 4 + e] = -lb[e];
-        di[8 * g + e] = -da[e];
-        di[8 * g + 4 + e] = -db[e];
+        si[8 * g + e] = la[e];
+        si[8 * g + 4 + e] = lb[e];
+        di[8 * g + e] = da[e];
+        di[8 * g + 4 + e] = db[e];
       }
     }
   };
@@ -433,8 +434,8 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   const int qpos = hs.q_pos0 + qt * kQQ + wave * 32 + l32;
   const int tile_first_q = hs.q_pos0 + qt * kQQ;
   const long long lrow = (long long)bh * p.Sq + qr;
-  const float lse2 = p.lse[lrow];  // lse * log2e (written by the preprocess kernel)
-  const float dlt = p.delta[lrow];
+  const float nlse2 = p.lse[lrow];  // -lse * log2e (written by the preprocess kernel)
+  const float ndlt = p.delta[lrow];  // -Delta
 
   bf16x8 qreg[NKK], oreg[NKK];
   {
@@ -509,7 +510,7 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         sacc[mt][i] = 0.f;
-        dpacc[mt][i] = -dlt;
+        dpacc[mt][i] = ndlt;
       }
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
@@ -528,7 +529,7 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
         for (int e = 0; e < 2; ++e) {
           const int i = 8 * (kb & 1) + 2 * j + e;
           const int mt = kb >> 1;
-          float pv = fast_exp2(fmaf(sacc[mt][i], sl2, -lse2));
+          float pv = fast_exp2(fmaf(sacc[mt][i], sl2, nlse2));
           if (MASK) {
             const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
             if (kpos > qpos) pv = 0.f;
