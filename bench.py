@@ -7,7 +7,7 @@ schedule, key/value rotation through the double buffer on the side stream, the
 attention-step kernel on every host, and finalisation.  Inputs are resident in HBM before
 the timed region.  Prints ONE JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra] [--only NAMES]
 
 `value` is TFLOP/s of algorithmic work (4*B*H*D per visible (query, key) pair; causal
 masking halves the diagonal blocks and skips blocks above the diagonal).  The
@@ -97,6 +97,117 @@ def recorded_traffic():
     return int(fields["traffic_bytes_per_launch"])
 
 
+def run_extras(ra, torch, mk, g, D, steps, only):
+    """Secondary configurations, each a named section; `only` (a set of names) selects some."""
+    extra = {}
+    want = lambda name: only is None or name in only
+
+    if want("fwd_bwd"):
+        # forward + backward, B=1 S=16384 H=16 D=128, 8 hosts x 2048
+        B3, S3, H3, N3 = 1, 16384, 16, 8
+        q3, k3, v3, do3 = (mk(B3, S3, H3, D) for _ in range(4))
+        o3 = torch.empty_like(q3)
+        l3 = torch.empty((B3, H3, S3), dtype=torch.float32, device="cuda")
+        dq3, dk3, dv3 = torch.empty_like(q3), torch.empty_like(k3), torch.empty_like(v3)
+
+        def fb():
+            ra.ring_attn_fwd(q3, k3, v3, o3, l3, N3, True)
+            ra.ring_attn_bwd(q3, k3, v3, o3, l3, do3, dq3, dk3, dv3, N3, True)
+        ms3, _ = time_calls(fb, max(3, steps // 2), 2)
+        f3 = 4.0 * B3 * H3 * D * causal_pairs(S3) * 3.5
+        extra["fwd_bwd_S16384_H16"] = {"ms": round(ms3, 3), "tflops": round(f3 / ms3 / 1e9, 2),
+                                       "tokens_per_s": round(S3 / (ms3 * 1e-3), 1)}
+        del q3, k3, v3, do3, o3, dq3, dk3, dv3
+
+    c5, N5, H5 = 32768, 8, 32
+    if want("host7") or want("decode"):
+        k5, v5 = mk(1, N5 * c5, H5, D), mk(1, N5 * c5, H5, D)
+    if want("host7"):
+        # one host's share: host 7 of 8, 32768-token query block against 262144 keys
+        qb = mk(1, c5, H5, D)
+        ob = torch.empty_like(qb)
+        lb = torch.empty((1, H5, c5), dtype=torch.float32, device="cuda")
+        ms5, _ = time_calls(lambda: ra.ring_attn_fwd_host(qb, k5, v5, ob, lb, N5, 7, True), 3, 1)
+        f5 = 4.0 * H5 * D * host_pairs(c5, 7, N5)
+        extra["host7_of_8_c32768_H32"] = {"ms": round(ms5, 3), "tflops": round(f5 / ms5 / 1e9, 2),
+                                          "query_tokens_per_s": round(c5 / (ms5 * 1e-3), 1)}
+        del qb, ob, lb
+    if want("decode"):
+        # ring decode against the same 262144-token cache (8 hosts x 32768), 1 and 8 new tokens
+        for tq in (1, 8):
+            qd = mk(1, tq, H5, D)
+            od = torch.empty_like(qd)
+            ld = torch.empty((1, H5, tq), dtype=torch.float32, device="cuda")
+            dec = lambda: ra.ring_attn_decode(qd, k5, v5, od, ld, N5, True)
+            for _ in range(3):
+                dec()
+            torch.cuda.synchronize()
+            ra.timing_read(ra.KERNEL_DECODE)
+            ra.timing_enable(True)
+            msd, _ = time_calls(dec, 20, 0)
+            ra.timing_enable(False)
+            kd, nd = ra.timing_read(ra.KERNEL_DECODE)
+            kv_bytes = 2.0 * N5 * c5 * H5 * D * 2
+            extra["decode_S262144_H32_Tq%d" % tq] = {
+                "ms": round(msd, 4), "partial_kernel_ms": round(kd / nd, 4),
+                "kv_GBps": round(kv_bytes / (kd / nd) / 1e6, 1),
+                "pct_hbm_8TBps": round(100.0 * kv_bytes / (kd / nd) / 1e6 / 8000.0, 1),
+                "tokens_per_s": round(tq / (msd * 1e-3), 1)}
+    if want("host7") or want("decode"):
+        del k5, v5
+
+    # d_model 4096 (32 heads of 128), S = 65536 in 8 host blocks of 8192
+    S4, dm, dff, H4, N4 = 65536, 4096, 16384, 32, 8
+    w = lambda *shape: (torch.randn(*shape, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    fatt = 4.0 * H4 * 128 * causal_pairs(S4)
+    if want("ffn") or want("layer"):
+        x4, dz4 = mk(S4, dm), mk(S4, dm)
+        w1, w2 = w(dm, dff), w(dff, dm)
+    if want("ffn"):
+        # blockwise FFN, d_ff 16384
+        y4 = torch.empty_like(x4)
+        msf, _ = time_calls(lambda: ra.blockwise_ffn(x4, w1, None, w2, None, y4, S4 // N4), 3, 1)
+        fffn = 2.0 * 2 * S4 * dm * dff
+        extra["ffn_fwd_T65536_d4096_ff16384"] = {"ms": round(msf, 3), "tflops": round(fffn / msf / 1e9, 2)}
+        del y4
+    if want("layer"):
+        # the Algorithm 1 layer, forward + backward
+        wq, wk, wv, wo = (w(dm, dm) for _ in range(4))
+        z4, dx4 = torch.empty_like(x4), torch.empty_like(x4)
+        f32 = lambda *shape: torch.empty(*shape, dtype=torch.float32, device="cuda")
+        dws = [f32(dm, dm) for _ in range(4)] + [f32(dm, dff), f32(dff, dm)]
+
+        def layer():
+            ra.ring_layer_fwd(x4, wq, wk, wv, wo, w1, w2, z4, H4, N4, True)
+            ra.ring_layer_bwd(x4, wq, wk, wv, wo, w1, w2, dz4, dx4, *dws, H4, N4, True)
+        msl, _ = time_calls(layer, 2, 1)
+        flayer = 3.5 * fatt + 3 * 24.0 * S4 * dm * dm  # attention fwd+bwd, GEMMs fwd (24 S h^2) + bwd (2x)
+        extra["layer_fwd_bwd_S65536_d4096"] = {"ms": round(msl, 3), "tflops": round(flayer / msl / 1e9, 2),
+                                               "tokens_per_s": round(S4 / (msl * 1e-3), 1),
+                                               "note": "algorithmic flops; backward recomputes the forward"}
+        del wq, wk, wv, wo, z4, dx4, dws
+    if want("ffn") or want("layer"):
+        del x4, dz4, w1, w2
+    if want("llama"):
+        # training step of a 2-layer LLaMA-7B-width stack (RMSNorm, RoPE, SwiGLU d_ff 11008,
+        # pre-norm) around ring attention, full recomputation
+        nl, dffl = 2, 11008
+        xl, dzl = mk(S4, dm), mk(S4, dm)
+        gain = lambda: (1.0 + 0.1 * torch.randn(dm, generator=g, device="cuda")).to(torch.bfloat16)
+        params = [[gain(), w(dm, dm), w(dm, dm), w(dm, dm), w(dm, dm), gain(), w(dm, dffl), w(dm, dffl), w(dffl, dm)]
+                  for _ in range(nl)]
+        grads = [[torch.empty(t.shape, dtype=torch.float32, device="cuda") for t in p] for p in params]
+        zl, dxl = torch.empty_like(xl), torch.empty_like(xl)
+        msll, _ = time_calls(lambda: ra.llama_stack_train_step(xl, params, dzl, zl, dxl, grads, H4, N4), 2, 1)
+        gemm_fwd = 2.0 * S4 * (4 * dm * dm + 3 * dm * dffl)
+        fll = nl * (3 * gemm_fwd + 3.5 * fatt)
+        extra["llama_stack2_train_step_S65536_d4096_ff11008"] = {
+            "ms": round(msll, 2), "tflops": round(fll / msll / 1e9, 2), "tokens_per_s": round(S4 / (msll * 1e-3), 1),
+            "note": "algorithmic flops (GEMMs fwd + 2x bwd, attention fwd + 2.5x bwd); the backward recomputes "
+                    "each layer's forward"}
+    return extra
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,6 +215,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="skip the secondary configurations")
+    ap.add_argument("--only", default=None,
+                    help="comma-separated secondary configurations to run alone (fwd_bwd, host7, decode, ffn, "
+                         "layer, llama): no main workload, prints {\"extra\": ...}; for profiling")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU's share of the virtual ring; --gpus %d is not "
@@ -117,6 +231,10 @@ def main():
     g = torch.Generator(device="cuda")
     g.manual_seed(2)
     mk = lambda *shape: torch.randn(*shape, generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    if args.only:
+        print(json.dumps({"extra": run_extras(ra, torch, mk, g, D, args.steps, set(args.only.split(",")))}),
+              flush=True)
+        return
     q, k, v = mk(B, S, H, D), mk(B, S, H, D), mk(B, S, H, D)
     o = torch.empty_like(q)
     lse = torch.empty((B, H, S), dtype=torch.float32, device="cuda")
@@ -161,96 +279,7 @@ def main():
     }
 
     if not args.no_extra:
-        extra = {}
-        # forward + backward, B=1 S=16384 H=16 D=128, 8 hosts x 2048
-        B3, S3, H3, N3 = 1, 16384, 16, 8
-        q3, k3, v3, do3 = (mk(B3, S3, H3, D) for _ in range(4))
-        o3 = torch.empty_like(q3)
-        l3 = torch.empty((B3, H3, S3), dtype=torch.float32, device="cuda")
-        dq3, dk3, dv3 = torch.empty_like(q3), torch.empty_like(k3), torch.empty_like(v3)
-
-        def fb():
-            ra.ring_attn_fwd(q3, k3, v3, o3, l3, N3, True)
-            ra.ring_attn_bwd(q3, k3, v3, o3, l3, do3, dq3, dk3, dv3, N3, True)
-        ms3, _ = time_calls(fb, max(3, args.steps // 2), 2)
-        f3 = 4.0 * B3 * H3 * D * causal_pairs(S3) * 3.5
-        extra["fwd_bwd_S16384_H16"] = {"ms": round(ms3, 3), "tflops": round(f3 / ms3 / 1e9, 2),
-                                       "tokens_per_s": round(S3 / (ms3 * 1e-3), 1)}
-        del q3, k3, v3, do3, o3, dq3, dk3, dv3
-        # one host's share: host 7 of 8, 32768-token query block against 262144 keys
-        c5, N5, H5 = 32768, 8, 32
-        qb = mk(1, c5, H5, D)
-        k5, v5 = mk(1, N5 * c5, H5, D), mk(1, N5 * c5, H5, D)
-        ob = torch.empty_like(qb)
-        lb = torch.empty((1, H5, c5), dtype=torch.float32, device="cuda")
-        ms5, _ = time_calls(lambda: ra.ring_attn_fwd_host(qb, k5, v5, ob, lb, N5, 7, True), 3, 1)
-        f5 = 4.0 * H5 * D * host_pairs(c5, 7, N5)
-        extra["host7_of_8_c32768_H32"] = {"ms": round(ms5, 3), "tflops": round(f5 / ms5 / 1e9, 2),
-                                          "query_tokens_per_s": round(c5 / (ms5 * 1e-3), 1)}
-        # ring decode against the same 262144-token cache (8 hosts x 32768), 1 and 8 new tokens
-        for tq in (1, 8):
-            qd = mk(1, tq, H5, D)
-            od = torch.empty_like(qd)
-            ld = torch.empty((1, H5, tq), dtype=torch.float32, device="cuda")
-            dec = lambda: ra.ring_attn_decode(qd, k5, v5, od, ld, N5, True)
-            for _ in range(3):
-                dec()
-            torch.cuda.synchronize()
-            ra.timing_read(ra.KERNEL_DECODE)
-            ra.timing_enable(True)
-            msd, _ = time_calls(dec, 20, 0)
-            ra.timing_enable(False)
-            kd, nd = ra.timing_read(ra.KERNEL_DECODE)
-            kv_bytes = 2.0 * N5 * c5 * H5 * D * 2
-            extra["decode_S262144_H32_Tq%d" % tq] = {
-                "ms": round(msd, 4), "partial_kernel_ms": round(kd / nd, 4),
-                "kv_GBps": round(kv_bytes / (kd / nd) / 1e6, 1),
-                "pct_hbm_8TBps": round(100.0 * kv_bytes / (kd / nd) / 1e6 / 8000.0, 1),
-                "tokens_per_s": round(tq / (msd * 1e-3), 1)}
-        del qb, k5, v5, ob, lb
-        # blockwise FFN and the full layer (forward + backward) at d_model 4096, d_ff 16384,
-        # S = 65536 in 8 host blocks of 8192, 32 heads of 128
-        S4, dm, dff, H4, N4 = 65536, 4096, 16384, 32, 8
-        w = lambda *shape: (torch.randn(*shape, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
-        x4, dz4 = mk(S4, dm), mk(S4, dm)
-        wq, wk, wv, wo = (w(dm, dm) for _ in range(4))
-        w1, w2 = w(dm, dff), w(dff, dm)
-        y4 = torch.empty_like(x4)
-        msf, _ = time_calls(lambda: ra.blockwise_ffn(x4, w1, None, w2, None, y4, S4 // N4), 3, 1)
-        fffn = 2.0 * 2 * S4 * dm * dff
-        extra["ffn_fwd_T65536_d4096_ff16384"] = {"ms": round(msf, 3), "tflops": round(fffn / msf / 1e9, 2)}
-        z4, dx4 = torch.empty_like(x4), torch.empty_like(x4)
-        f32 = lambda *shape: torch.empty(*shape, dtype=torch.float32, device="cuda")
-        dws = [f32(dm, dm) for _ in range(4)] + [f32(dm, dff), f32(dff, dm)]
-
-        def layer():
-            ra.ring_layer_fwd(x4, wq, wk, wv, wo, w1, w2, z4, H4, N4, True)
-            ra.ring_layer_bwd(x4, wq, wk, wv, wo, w1, w2, dz4, dx4, *dws, H4, N4, True)
-        msl, _ = time_calls(layer, 2, 1)
-        fatt = 4.0 * H4 * 128 * causal_pairs(S4)
-        flayer = 3.5 * fatt + 3 * 24.0 * S4 * dm * dm  # attention fwd+bwd, GEMMs fwd (24 S h^2) + bwd (2x)
-        extra["layer_fwd_bwd_S65536_d4096"] = {"ms": round(msl, 3), "tflops": round(flayer / msl / 1e9, 2),
-                                               "tokens_per_s": round(S4 / (msl * 1e-3), 1),
-                                               "note": "algorithmic flops; backward recomputes the forward"}
-        del x4, dz4, wq, wk, wv, wo, w1, w2, y4, z4, dx4, dws
-        # training step of a 2-layer LLaMA-7B-width stack (RMSNorm, RoPE, SwiGLU d_ff 11008,
-        # pre-norm) around ring attention, S = 65536 in 8 host blocks, full recomputation
-        nl, dffl = 2, 11008
-        xl, dzl = mk(S4, dm), mk(S4, dm)
-        gain = lambda: (1.0 + 0.1 * torch.randn(dm, generator=g, device="cuda")).to(torch.bfloat16)
-        params = [[gain(), w(dm, dm), w(dm, dm), w(dm, dm), w(dm, dm), gain(), w(dm, dffl), w(dm, dffl), w(dffl, dm)]
-                  for _ in range(nl)]
-        grads = [[torch.empty(t.shape, dtype=torch.float32, device="cuda") for t in p] for p in params]
-        zl, dxl = torch.empty_like(xl), torch.empty_like(xl)
-        msll, _ = time_calls(lambda: ra.llama_stack_train_step(xl, params, dzl, zl, dxl, grads, H4, N4), 2, 1)
-        gemm_fwd = 2.0 * S4 * (4 * dm * dm + 3 * dm * dffl)
-        fll = nl * (3 * gemm_fwd + 3.5 * fatt)
-        extra["llama_stack2_train_step_S65536_d4096_ff11008"] = {
-            "ms": round(msll, 2), "tflops": round(fll / msll / 1e9, 2), "tokens_per_s": round(S4 / (msll * 1e-3), 1),
-            "note": "algorithmic flops (GEMMs fwd + 2x bwd, attention fwd + 2.5x bwd); the backward recomputes "
-                    "each layer's forward"}
-        out["extra"] = extra
-
+        out["extra"] = run_extras(ra, torch, mk, g, D, args.steps, None)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(B, S, H, D)
     print(json.dumps(out), flush=True)
