@@ -2,12 +2,14 @@
 //
 // C[M][N] = sum_k A[m][k] B[k][n] with A stored row-major [M][K] (TA = 0) or as its
 // transpose [K][M] (TA = 1), B stored row-major [K][N] (TB = 0) or as [N][K] (TB = 1).
-// Workgroup tile 256 x 256, K step 64, 4 waves each owning a 128 x 128 sub-tile
-// (16 accumulators of 32 x 32).  Tiles are staged through LDS in their memory layout
-// (double buffered); an operand whose registers must run along its contiguous
-// dimension is read with the LDS transpose read.  Each wave computes C^T = B^T A^T so
-// that a lane owns one row m of C and four consecutive columns n per register group:
-// epilogues then read bias / residual / pre-activation and write C with vector accesses.
+// Workgroup tile 256 x 256, 4 waves each owning a 128 x 128 sub-tile (16 accumulators of
+// 32 x 32).  K advances 32 at a time through a ring of five LDS stages (all 160 KB of
+// the CU's LDS) filled by direct-to-LDS buffer loads four steps ahead of their use.  Tiles are kept in their
+// memory layout, unpadded, with 16-byte chunks XOR-swizzled per row so that both the row
+// reads and the transpose reads (an operand whose registers must run along its contiguous
+// dimension) are free of bank conflicts.  Each wave computes C^T = B^T A^T so that a lane
+// owns one row m of C and four consecutive columns n per register group: epilogues then
+// read bias / residual / pre-activation and write C with vector accesses.
 #include "ra_common.h"
 #include "ra_gemm.h"
 #include "ringattn.h"
@@ -15,7 +17,31 @@
 namespace ra {
 namespace {
 
-constexpr int kTM = 256, kTN = 256, kTK = 64, kGT = 256;
+constexpr int kTM = 256, kTN = 256, kTK = 32, kGT = 256;
+constexpr int kNS = 5;                      // ring stages
+constexpr int kTileB = 256 * kTK * 2;       // bytes of one operand tile (16 KB)
+constexpr int kLoadsPerTile = kTileB / 1024 / (kGT / 64);  // 1 KB loads per wave per tile
+
+// Tile layouts in LDS (no padding; chunk = 16 bytes = 8 elements):
+//   row tile   [256][32] (A with TA = 0, B with TB = 1): 64-byte rows of 4 chunks, logical
+//              chunk c of row r stored at c ^ ((r >> 2) & 3);
+//   k-major    [32][256] (A with TA = 1, B with TB = 0): 512-byte rows of 32 chunks,
+//              logical chunk c of row r stored at c ^ (4 (r & 3)).
+// A one-wave direct-to-LDS load fills 1 KB: 16 rows of a row tile, or 2 rows of a k-major
+// tile, lane i landing at byte 16 i; the swizzle is applied to the global address.
+__device__ __forceinline__ int swz_row(int r) { return (r >> 2) & 3; }
+
+// Direct-to-LDS load of 16 bytes per lane (lane i lands at byte 16 i of the wave-uniform
+// LDS address lds_addr), issued from inline assembly so that the compiler does not track
+// it: the main loop waits for these loads itself, with counts that let the loads of later
+// stages stay in flight (the compiler's own tracking of such loads would wait for all of
+// them before reading any stage).  M0 carries the LDS address; no compiler-generated code
+// in this kernel uses M0.
+__device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rsrc, unsigned lds_addr, int voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_addr), "v"(voff), "s"(rsrc)
+               : "memory");
+}
+__device__ __forceinline__ int swz_kmaj(int r) { return 4 * (r & 3); }
 
 template <int ACT>
 __device__ __forceinline__ float act_apply(float h) {
@@ -46,23 +72,23 @@ __device__ __forceinline__ float act_grad(float h) {
   return cdf + h * pdf;
 }
 
-template <bool TA, bool TB>
-struct TileShape {
-  // LDS tiles kept in memory layout: rows x (cols + pad) elements
-  static constexpr int A_ROWS = TA ? kTK : kTM, A_COLS = TA ? kTM : kTK, A_LD = A_COLS + (TA ? 16 : 8);
-  static constexpr int B_ROWS = TB ? kTN : kTK, B_COLS = TB ? kTK : kTN, B_LD = B_COLS + (TB ? 8 : 16);
-  static constexpr int A_ELEMS = A_ROWS * A_LD, B_ELEMS = B_ROWS * B_LD;
-  static constexpr int A_CHUNKS = A_ROWS * A_COLS / 8 / kGT;  // 16-byte chunks per thread
-  static constexpr int B_CHUNKS = B_ROWS * B_COLS / 8 / kGT;
-};
 
 // ACT: the activation of the ACT epilogues (an ra_act value, fixed at compile time so
 // that each kernel holds the code of one activation only).
 template <bool TA, bool TB, int EPI, int ACT>
 __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
-  using TS = TileShape<TA, TB>;
-  extern __shared__ __attribute__((aligned(16))) bf16 smem[];
-  // buffer b of A at smem + b*A_ELEMS; buffer b of B at smem + 2*A_ELEMS + b*B_ELEMS
+  // one LDS object per stage (A tile, then B tile), so that reads of one stage are known not
+  // to alias the direct-to-LDS loads in flight into the others
+  __shared__ __attribute__((aligned(1024))) char sS0[2 * kTileB];
+  __shared__ __attribute__((aligned(1024))) char sS1[2 * kTileB];
+  __shared__ __attribute__((aligned(1024))) char sS2[2 * kTileB];
+  __shared__ __attribute__((aligned(1024))) char sS3[2 * kTileB];
+  __shared__ __attribute__((aligned(1024))) char sS4[2 * kTileB];
+  auto stage = [&](auto Sc) __attribute__((always_inline)) -> char* {
+    constexpr int S = decltype(Sc)::value % kNS;
+    if constexpr (S == 0) return sS0; else if constexpr (S == 1) return sS1; else if constexpr (S == 2) return sS2;
+    else if constexpr (S == 3) return sS3; else return sS4;
+  };
 
   // tile order: XCD-contiguous ranges, then groups of 8 tile-rows sweeping across N
   const int tiles_m = g.M / kTM, tiles_n = g.N / kTN;
@@ -80,6 +106,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
   const int wm = wave >> 1, wn = wave & 1;
   const bf16* A = (const bf16*)g.A;
   const bf16* B = (const bf16*)g.B;
+  const int nk = g.K / kTK;
 
   f32x16 acc[4][4];  // [n tile][m tile] of C^T
 #pragma unroll
@@ -89,148 +116,226 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
 
-  u32x4 apre[TS::A_CHUNKS], bpre[TS::B_CHUNKS];
-  auto gload = [&](int kt) {
-    const int k0 = kt * kTK;
-#pragma unroll
-    for (int c = 0; c < TS::A_CHUNKS; ++c) {
-      const int ch = tid + c * kGT;
-      const int r = ch / (TS::A_COLS / 8), col = (ch % (TS::A_COLS / 8)) * 8;
-      const long long off = TA ? (long long)(k0 + r) * g.lda + m0 + col : (long long)(m0 + r) * g.lda + k0 + col;
-      apre[c] = *(const u32x4*)(A + off);
+  // ---- direct-to-LDS loads: per-lane byte offsets from the tile origin (fixed), and
+  // the tile origin, which moves by kTK along K (scalar) ------------------------------
+  // load j of this wave fills LDS bytes [(wave * kLoadsPerTile + j) * 1024, +1024)
+  auto lane_off = [&](bool kmajor, long long ld, int j) __attribute__((always_inline)) -> int {
+    const int blk = wave * kLoadsPerTile + j;
+    if (!kmajor) {  // 16 rows x 4 chunks
+      const int r = blk * 16 + (lane >> 2), pc = lane & 3;
+      return (int)(2 * (r * ld + 8 * (pc ^ swz_row(r))));
     }
-#pragma unroll
-    for (int c = 0; c < TS::B_CHUNKS; ++c) {
-      const int ch = tid + c * kGT;
-      const int r = ch / (TS::B_COLS / 8), col = (ch % (TS::B_COLS / 8)) * 8;
-      const long long off = TB ? (long long)(n0 + r) * g.ldb + k0 + col : (long long)(k0 + r) * g.ldb + n0 + col;
-      bpre[c] = *(const u32x4*)(B + off);
-    }
+    const int r = blk * 2 + (lane >> 5), pc = lane & 31;  // 2 rows x 32 chunks
+    return (int)(2 * (r * ld + 8 * (pc ^ swz_kmaj(r))));
   };
-  auto lstore = [&](int buf) {
+  int aoff[kLoadsPerTile], boff[kLoadsPerTile];
 #pragma unroll
-    for (int c = 0; c < TS::A_CHUNKS; ++c) {
-      const int ch = tid + c * kGT;
-      const int r = ch / (TS::A_COLS / 8), col = (ch % (TS::A_COLS / 8)) * 8;
-      *(u32x4*)(smem + buf * TS::A_ELEMS + r * TS::A_LD + col) = apre[c];
-    }
-#pragma unroll
-    for (int c = 0; c < TS::B_CHUNKS; ++c) {
-      const int ch = tid + c * kGT;
-      const int r = ch / (TS::B_COLS / 8), col = (ch % (TS::B_COLS / 8)) * 8;
-      *(u32x4*)(smem + 2 * TS::A_ELEMS + buf * TS::B_ELEMS + r * TS::B_LD + col) = bpre[c];
-    }
-  };
-
-  const int gq = lane >> 4, li = lane & 15;
-  const int tcol = 16 * (gq & 1) + 4 * (li & 3);  // transpose-read column offset
-  const int trow = 8 * hi + (li >> 2);            // transpose-read row offset
-  const int nk = g.K / kTK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    const bf16* a_s = smem + buf * TS::A_ELEMS;
-    const bf16* b_s = smem + 2 * TS::A_ELEMS + buf * TS::B_ELEMS;
-#pragma unroll
-    for (int kk = 0; kk < kTK / 16; ++kk) {
-      bf16x8 bop[4], aop[4];
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const int nb = wn * 128 + 32 * ni;
-        if (TB) {
-          bop[ni] = *(const bf16x8*)(b_s + (nb + l32) * TS::B_LD + 16 * kk + 8 * hi);
-        } else {
-          const bf16* p = b_s + (16 * kk + trow) * TS::B_LD + nb + tcol;
-          const bf16x4 lo = lds_read_tr16(p), up = lds_read_tr16(p + 4 * TS::B_LD);
-          bop[ni] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-        }
-      }
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
-        const int mb = wm * 128 + 32 * mi;
-        if (!TA) {
-          aop[mi] = *(const bf16x8*)(a_s + (mb + l32) * TS::A_LD + 16 * kk + 8 * hi);
-        } else {
-          const bf16* p = a_s + (16 * kk + trow) * TS::A_LD + mb + tcol;
-          const bf16x4 lo = lds_read_tr16(p), up = lds_read_tr16(p + 4 * TS::A_LD);
-          aop[mi] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-        }
-      }
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni)
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi) acc[ni][mi] = mfma32(bop[ni], aop[mi], acc[ni][mi]);
-    }
-    if (kt + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
+  for (int j = 0; j < kLoadsPerTile; ++j) {
+    aoff[j] = lane_off(TA, g.lda, j);
+    boff[j] = lane_off(!TB, g.ldb, j);
   }
+  // extent of a tile's reads (bytes from its origin), for the buffer descriptors
+  const int a_ext = (int)(2 * (TA ? (long long)(kTK - 1) * g.lda + kTM : (long long)(kTM - 1) * g.lda + kTK));
+  const int b_ext = (int)(2 * (TB ? (long long)(kTN - 1) * g.ldb + kTK : (long long)(kTK - 1) * g.ldb + kTN));
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  auto load_stage = [&](int kt, auto Sc) __attribute__((always_inline)) {
+    const int k0 = kt * kTK;
+    const bf16* at = TA ? A + (long long)k0 * g.lda + m0 : A + (long long)m0 * g.lda + k0;
+    const bf16* bt = TB ? B + (long long)n0 * g.ldb + k0 : B + (long long)k0 * g.ldb + n0;
+    const __amdgpu_buffer_rsrc_t ra_ = __builtin_amdgcn_make_buffer_rsrc((void*)at, (short)0, a_ext, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rb_ = __builtin_amdgcn_make_buffer_rsrc((void*)bt, (short)0, b_ext, 0x00020000);
+    const unsigned st = (unsigned)(unsigned long long)(lds_void*)stage(Sc) + wave_u * kLoadsPerTile * 1024;
+#pragma unroll
+    for (int j = 0; j < kLoadsPerTile; ++j) {
+      dma16(ra_, st + j * 1024, aoff[j]);
+      dma16(rb_, st + kTileB + j * 1024, boff[j]);
+    }
+  };
 
-  // ---- epilogue: lane owns row m, registers 4g..4g+3 hold columns n0..n0+3 ----------
+  // ---- LDS read offsets (bytes within an operand tile) --------------------------------
+  // row-tile operand: rows base + l32 (base a multiple of 32), logical chunk 2 kk + hi
+  int roff[2];
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi) {
-    const int m = m0 + wm * 128 + 32 * mi + l32;
+  for (int kk = 0; kk < 2; ++kk) roff[kk] = l32 * 64 + 16 * ((2 * kk + hi) ^ swz_row(l32));
+  // k-major operand by transpose reads: rows 16 kk + 8 hi + li / 4 (and + 4), columns
+  // base + 32 t + 16 (gq & 1) + 4 (li & 3) for t = 0..3 (base a multiple of 128)
+  const int gq = lane >> 4, li = lane & 15;
+  const int trow = 8 * hi + (li >> 2);
+  int toff[4];
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni)
+  for (int t = 0; t < 4; ++t) {
+    const int col = 32 * t + 16 * (gq & 1) + 4 * (li & 3);
+    toff[t] = trow * 512 + 16 * ((col >> 3) ^ swz_kmaj(trow)) + 2 * (col & 7);
+  }
+  // operand fetch for k-slice kk of a stage: A operand rows m (bop: B^T rows n)
+  auto fetch = [&](const char* st, int kk, bf16x8* aop, bf16x8* bop) __attribute__((always_inline)) {
+    const char* as = st;
+    const char* bs = st + kTileB;
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const int n = n0 + wn * 128 + 32 * ni + 8 * q4 + 4 * hi;
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[ni][mi][4 * q4 + e];
-        const long long off = (long long)m * g.ldc + n;
-        if (EPI == EPI_BF16 || EPI == EPI_ACT_BF16 || EPI == EPI_ACT_STORE_H) {
-          if (g.bias) {
-            const bf16x4 bb = *(const bf16x4*)((const bf16*)g.bias + n);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += (float)bb[e];
-          }
-          if (EPI == EPI_ACT_STORE_H) *(f32x4*)(g.aux_f32 + off) = f32x4{v[0], v[1], v[2], v[3]};
-          if (EPI != EPI_BF16) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = act_apply<ACT>(v[e]);
-          }
-          if (g.residual) {
-            const bf16x4 rr = *(const bf16x4*)((const bf16*)g.residual + off);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] += (float)rr[e];
-          }
-          *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        } else if (EPI == EPI_ACT_GRAD_BF16) {
-          const f32x4 h = *(const f32x4*)(g.aux_f32 + off);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] *= act_grad<ACT>(h[e]);
-          *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        } else if (EPI == EPI_GLU_BF16) {
-          const f32x4 u = *(const f32x4*)(g.aux_f32 + off);
-          if (g.aux2_f32) *(f32x4*)(g.aux2_f32 + off) = f32x4{v[0], v[1], v[2], v[3]};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] *= u[e] * sigmoid_f(u[e]);
-          *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-        } else if (EPI == EPI_GLU_GRAD) {
-          const f32x4 u = *(const f32x4*)(g.aux_f32 + off);
-          const f32x4 w = *(const f32x4*)(g.aux2_f32 + off);
-          float du[4], dw[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float sg = sigmoid_f(u[e]);
-            du[e] = v[e] * w[e] * sg * (1.f + u[e] * (1.f - sg));
-            dw[e] = v[e] * u[e] * sg;
-          }
-          *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(du[0], du[1]), pack_bf16x2(du[2], du[3])};
-          *(u32x2*)((bf16*)g.C2 + off) = u32x2{pack_bf16x2(dw[0], dw[1]), pack_bf16x2(dw[2], dw[3])};
-        } else {  // EPI_F32: overwrite, or add into C
-          f32x4* cp = (f32x4*)((float*)g.C + off);
-          if (g.accumulate) {
-            const f32x4 c = *cp;
-            *cp = f32x4{c[0] + v[0], c[1] + v[1], c[2] + v[2], c[3] + v[3]};
-          } else {
-            *cp = f32x4{v[0], v[1], v[2], v[3]};
-          }
-        }
+    for (int i = 0; i < 4; ++i) {
+      if (!TA) {
+        aop[i] = *(const bf16x8*)(as + (wm * 128 + 32 * i) * 64 + roff[kk]);
+      } else {
+        const char* p = as + kk * 16 * 512 + wm * 256 + toff[i];
+        const bf16x4 lo = lds_read_tr16((const bf16*)p), up = lds_read_tr16((const bf16*)(p + 4 * 512));
+        aop[i] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
       }
+      if (TB) {
+        bop[i] = *(const bf16x8*)(bs + (wn * 128 + 32 * i) * 64 + roff[kk]);
+      } else {
+        const char* p = bs + kk * 16 * 512 + wn * 256 + toff[i];
+        const bf16x4 lo = lds_read_tr16((const bf16*)p), up = lds_read_tr16((const bf16*)(p + 4 * 512));
+        bop[i] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+      }
+    }
+  };
+  auto mfmas = [&](const bf16x8* aop, const bf16x8* bop, int n0i, int n1i) __attribute__((always_inline)) {
+#pragma unroll
+    for (int ni = n0i; ni < n1i; ++ni)
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) acc[ni][mi] = mfma32(bop[ni], aop[mi], acc[ni][mi]);
+  };
+
+  // ---- main loop ----------------------------------------------------------------------
+  // Step kt (stage kt % 5): issue the loads of step kt+4 into the stage step kt-1 used;
+  // slice 0's products while slice 1's operands are read; then wait for step kt+1's loads
+  // (those of kt+2 .. kt+4 may stay in flight -- loads complete in issue order), the
+  // barrier (every read of this stage has been issued by now), and step kt+1's slice-0
+  // reads, covered by slice 1's products.
+  bf16x8 a0[4], b0[4], a1[4], b1[4];
+#pragma unroll
+  for (int s = 0; s < kNS - 1; ++s)
+    if (s < nk) {
+      if (s == 0) load_stage(s, std::integral_constant<int, 0>{});
+      if (s == 1) load_stage(s, std::integral_constant<int, 1>{});
+      if (s == 2) load_stage(s, std::integral_constant<int, 2>{});
+      if (s == 3) load_stage(s, std::integral_constant<int, 3>{});
+    }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  fetch(sS0, 0, a0, b0);
+  auto step = [&](auto Sc, int kt) __attribute__((always_inline)) {
+    constexpr int S = decltype(Sc)::value;
+    if (kt + kNS - 1 < nk) load_stage(kt + kNS - 1, std::integral_constant<int, (S + kNS - 1) % kNS>{});
+    fetch(stage(Sc), 1, a1, b1);
+    mfmas(a0, b0, 0, 4);
+    // step kt+1 must have landed: at most the loads of steps kt+2 .. kt+4 outstanding
+    constexpr int LPS = 2 * kLoadsPerTile;  // loads per step per wave
+    if (kt + 4 < nk)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * LPS) : "memory");
+    else if (kt + 3 < nk)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPS) : "memory");
+    else if (kt + 2 < nk)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPS) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+    if (kt + 1 < nk) fetch(stage(std::integral_constant<int, S + 1>{}), 0, a0, b0);
+    mfmas(a1, b1, 0, 4);
+  };
+  int kt = 0;
+  for (; kt + kNS - 1 < nk; kt += kNS) {
+    step(std::integral_constant<int, 0>{}, kt);
+    step(std::integral_constant<int, 1>{}, kt + 1);
+    step(std::integral_constant<int, 2>{}, kt + 2);
+    step(std::integral_constant<int, 3>{}, kt + 3);
+    step(std::integral_constant<int, 4>{}, kt + 4);
+  }
+  if (kt < nk) step(std::integral_constant<int, 0>{}, kt++);
+  if (kt < nk) step(std::integral_constant<int, 1>{}, kt++);
+  if (kt < nk) step(std::integral_constant<int, 2>{}, kt++);
+  if (kt < nk) step(std::integral_constant<int, 3>{}, kt++);
+
+  // ---- epilogue --------------------------------------------------------------------
+  // The float32 accumulators pass through LDS (the stage buffers are free now) in two
+  // passes of 128 rows: the two waves owning those rows write them, 32 rows per stage
+  // buffer (1 KB rows; 16-byte chunk c of row r stored at c ^ (r & 15), so both the
+  // writes -- 32 rows at one column -- and the row reads are free of bank conflicts);
+  // then every wave takes 8 rows of each buffer and a lane handles 4 consecutive columns,
+  // so bias, residual, pre-activation and output accesses are contiguous along rows.
+  auto epi4 = [&](int m, int n, float* v) __attribute__((always_inline)) {
+    const long long off = (long long)m * g.ldc + n;
+    if (EPI == EPI_BF16 || EPI == EPI_ACT_BF16 || EPI == EPI_ACT_STORE_H) {
+      if (g.bias) {
+        const bf16x4 bb = *(const bf16x4*)((const bf16*)g.bias + n);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] += (float)bb[e];
+      }
+      if (EPI == EPI_ACT_STORE_H) *(f32x4*)(g.aux_f32 + off) = f32x4{v[0], v[1], v[2], v[3]};
+      if (EPI != EPI_BF16) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = act_apply<ACT>(v[e]);
+      }
+      if (g.residual) {
+        const bf16x4 rr = *(const bf16x4*)((const bf16*)g.residual + off);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] += (float)rr[e];
+      }
+      *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    } else if (EPI == EPI_ACT_GRAD_BF16) {
+      const f32x4 h = *(const f32x4*)(g.aux_f32 + off);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] *= act_grad<ACT>(h[e]);
+      *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    } else if (EPI == EPI_GLU_BF16) {
+      const f32x4 u = *(const f32x4*)(g.aux_f32 + off);
+      if (g.aux2_f32) *(f32x4*)(g.aux2_f32 + off) = f32x4{v[0], v[1], v[2], v[3]};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] *= u[e] * sigmoid_f(u[e]);
+      *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    } else if (EPI == EPI_GLU_GRAD) {
+      const f32x4 u = *(const f32x4*)(g.aux_f32 + off);
+      const f32x4 w = *(const f32x4*)(g.aux2_f32 + off);
+      float du[4], dw[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float sg = sigmoid_f(u[e]);
+        du[e] = v[e] * w[e] * sg * (1.f + u[e] * (1.f - sg));
+        dw[e] = v[e] * u[e] * sg;
+      }
+      *(u32x2*)((bf16*)g.C + off) = u32x2{pack_bf16x2(du[0], du[1]), pack_bf16x2(du[2], du[3])};
+      *(u32x2*)((bf16*)g.C2 + off) = u32x2{pack_bf16x2(dw[0], dw[1]), pack_bf16x2(dw[2], dw[3])};
+    } else {  // EPI_F32: overwrite, or add into C
+      f32x4* cp = (f32x4*)((float*)g.C + off);
+      if (g.accumulate) {
+        const f32x4 c = *cp;
+        *cp = f32x4{c[0] + v[0], c[1] + v[1], c[2] + v[2], c[3] + v[3]};
+      } else {
+        *cp = f32x4{v[0], v[1], v[2], v[3]};
+      }
+    }
+  };
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    if (wm == pass) {
+      // lane: row 32 mi + l32 of the pass (stage buffer mi, local row l32), columns
+      // 128 wn + 32 ni + 8 q4 + 4 hi .. +3 (chunk 32 wn + 8 ni + 2 q4 + hi)
+      static_for<0, 4>([&](auto Mi) __attribute__((always_inline)) {
+        constexpr int mi = decltype(Mi)::value;
+        char* sb = stage(std::integral_constant<int, mi>{}) + l32 * 1024;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const int c = 32 * wn + 8 * ni + 2 * q4 + hi;
+            *(f32x4*)(sb + 16 * (c ^ (l32 & 15))) =
+                f32x4{acc[ni][mi][4 * q4], acc[ni][mi][4 * q4 + 1], acc[ni][mi][4 * q4 + 2], acc[ni][mi][4 * q4 + 3]};
+          }
+      });
+    }
+    __syncthreads();
+    static_for<0, 4>([&](auto Bi) __attribute__((always_inline)) {
+      constexpr int bi = decltype(Bi)::value;
+      const char* sb = stage(std::integral_constant<int, bi>{});
+#pragma unroll 2
+      for (int rr = 0; rr < 8; ++rr) {
+        const int lr = 8 * wave + rr;  // local row of the buffer
+        const f32x4 t = *(const f32x4*)(sb + lr * 1024 + 16 * (lane ^ (lr & 15)));
+        float v[4] = {t[0], t[1], t[2], t[3]};
+        epi4(m0 + 128 * pass + 32 * bi + lr, n0 + 4 * lane, v);
+      }
+    });
+    if (pass == 0) __syncthreads();
   }
 }
 
@@ -258,14 +363,8 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* part, fl
 
 template <bool TA, bool TB, int EPI, int ACT>
 hipError_t launch_t(const GemmArgs& g, hipStream_t st) {
-  using TS = TileShape<TA, TB>;
-  const size_t lds = (size_t)(2 * TS::A_ELEMS + 2 * TS::B_ELEMS) * sizeof(bf16);
-  // the tiles need more than the default dynamic LDS limit (set on the current device)
-  hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<TA, TB, EPI, ACT>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
   const int total = (g.M / kTM) * (g.N / kTN);
-  hipLaunchKernelGGL((gemm_kernel<TA, TB, EPI, ACT>), dim3(total), dim3(kGT), lds, st, g);
+  hipLaunchKernelGGL((gemm_kernel<TA, TB, EPI, ACT>), dim3(total), dim3(kGT), 0, st, g);
   return hipGetLastError();
 }
 
