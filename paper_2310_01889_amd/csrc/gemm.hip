@@ -11,6 +11,7 @@
 // owns one row m of C and four consecutive columns n per register group: epilogues then
 // read bias / residual / pre-activation and write C with vector accesses.
 #include "ra_common.h"
+#include "ra_dma.h"
 #include "ra_gemm.h"
 #include "ringattn.h"
 
@@ -30,17 +31,6 @@ constexpr int kLoadsPerTile = kTileB / 1024 / (kGT / 64);  // 1 KB loads per wav
 // A one-wave direct-to-LDS load fills 1 KB: 16 rows of a row tile, or 2 rows of a k-major
 // tile, lane i landing at byte 16 i; the swizzle is applied to the global address.
 __device__ __forceinline__ int swz_row(int r) { return (r >> 2) & 3; }
-
-// Direct-to-LDS load of 16 bytes per lane (lane i lands at byte 16 i of the wave-uniform
-// LDS address lds_addr), issued from inline assembly so that the compiler does not track
-// it: the main loop waits for these loads itself, with counts that let the loads of later
-// stages stay in flight (the compiler's own tracking of such loads would wait for all of
-// them before reading any stage).  M0 carries the LDS address; no compiler-generated code
-// in this kernel uses M0.
-__device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rsrc, unsigned lds_addr, int voff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_addr), "v"(voff), "s"(rsrc)
-               : "memory");
-}
 __device__ __forceinline__ int swz_kmaj(int r) { return 4 * (r & 3); }
 
 template <int ACT>
@@ -142,13 +132,12 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
     const int k0 = kt * kTK;
     const bf16* at = TA ? A + (long long)k0 * g.lda + m0 : A + (long long)m0 * g.lda + k0;
     const bf16* bt = TB ? B + (long long)n0 * g.ldb + k0 : B + (long long)k0 * g.ldb + n0;
-    const __amdgpu_buffer_rsrc_t ra_ = __builtin_amdgcn_make_buffer_rsrc((void*)at, (short)0, a_ext, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rb_ = __builtin_amdgcn_make_buffer_rsrc((void*)bt, (short)0, b_ext, 0x00020000);
-    const unsigned st = (unsigned)(unsigned long long)(lds_void*)stage(Sc) + wave_u * kLoadsPerTile * 1024;
+    const __amdgpu_buffer_rsrc_t ra_ = make_rsrc(at, a_ext), rb_ = make_rsrc(bt, b_ext);
+    const unsigned st = lds_addr(stage(Sc)) + wave_u * kLoadsPerTile * 1024;
 #pragma unroll
     for (int j = 0; j < kLoadsPerTile; ++j) {
-      dma16(ra_, st + j * 1024, aoff[j]);
-      dma16(rb_, st + kTileB + j * 1024, boff[j]);
+      dma_lds16(ra_, st + j * 1024, aoff[j]);  // tile loads the loop waits for itself
+      dma_lds16(rb_, st + kTileB + j * 1024, boff[j]);
     }
   };
 

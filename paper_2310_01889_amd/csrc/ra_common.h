@@ -68,16 +68,6 @@ __device__ __forceinline__ void buffer_load_lds4(const void* base, int num_bytes
 #endif
 }
 
-// Workgroup barrier that orders the waves' LDS instructions only: every LDS instruction
-// of the wave issued before it has completed, and (memory clobber) the compiler moves no
-// memory access across it.  Unlike __syncthreads() it does not wait for vector-memory
-// operations (a fence would, since direct-to-LDS loads count as pending LDS writes), so
-// tile loads issued earlier stay in flight; callers first wait, with an explicit vmcnt,
-// for the loads whose data the other waves will read after the barrier.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
 // Max / sum of a value with the same value in lane l ^ 32 (v_permlane32_swap).
 __device__ __forceinline__ float pair_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
