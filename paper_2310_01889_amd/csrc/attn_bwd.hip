@@ -129,13 +129,27 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   const int kpos = hs.k_pos0 + key_in_blk;
   const bf16* krow = (const bf16*)hs.k + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
   const bf16* vrow = (const bf16*)hs.v + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
+  // forwarding: the workgroup writes the rows of its 128 keys, as loaded, into the next
+  // host's receive slot for the next ring step (layout [B, c, H, D])
+  const int fto = p.fwd.to[slot];
+  bf16* fkrow = nullptr;
+  bf16* fvrow = nullptr;
+  if (fto >= 0) {
+    const long long off = (long long)fto * p.fwd.blk_bytes + 2 * (((long long)b * p.c + key_in_blk) * rs + h * D);
+    fkrow = (bf16*)((char*)p.fwd.k0 + off);
+    fvrow = (bf16*)((char*)p.fwd.v0 + off);
+  }
   bf16x8 kreg[NKK], vreg[NKK];
 #pragma unroll
   for (int kk = 0; kk < NKK; ++kk) {
     const bf16x8 kx = *(const bf16x8*)(krow + 16 * kk + 8 * hi);
+    vreg[kk] = *(const bf16x8*)(vrow + 16 * kk + 8 * hi);
+    if (fkrow) {
+      *(bf16x8*)(fkrow + 16 * kk + 8 * hi) = kx;
+      *(bf16x8*)(fvrow + 16 * kk + 8 * hi) = vreg[kk];
+    }
 #pragma unroll
     for (int e = 0; e < 8; ++e) kreg[kk][e] = (bf16)((float)kx[e] * sl2);  // scores in log2 units
-    vreg[kk] = *(const bf16x8*)(vrow + 16 * kk + 8 * hi);
   }
   f32x16 dkacc[NDT], dvacc[NDT];
 #pragma unroll

@@ -11,6 +11,19 @@ constexpr int kMaxSlots = 64;        // hosts per launch (= maximum ring size)
 constexpr int kFirst = 1;            // host's first active step: start from m=-inf, l=0, acc=0
 constexpr int kLast = 2;             // host's last active step: finalize o = acc / l, lse
 
+// Forwarding of the key/value block a host holds to the host that needs it at the next
+// ring step (host i at step t holds block j = (i - t) mod N, which host i+1 holds at step
+// t+1).  The bf16 backward step kernels copy the block's rows, while they have them in
+// hand, into that host's receive slot for the next step: slot s of the next step's half of
+// the receive buffers starts at k0 + s * blk_bytes (v0 for values), in the layout
+// [B, c, H, D].  to[n] is the destination slot of launch slot n, or -1 (no forwarding).
+struct StepForward {
+  const void* k0;
+  const void* v0;
+  long long blk_bytes;
+  signed char to[kMaxSlots];
+};
+
 // One host's work in one ring step.
 struct StepHost {
   const void* k;          // key block, row 0 (batch 0, head 0)
@@ -51,6 +64,8 @@ struct BwdStep {
   long long dkv_bstride;  // Skv * H * D
   int n_slots, B, H, Sq, c, causal;
   float scale;
+  StepForward fwd;        // bf16 dK/dV kernel only: forward each slot's block (the keys a
+                          // workgroup holds) to the next host
 };
 
 hipError_t launch_fwd_bf16(const FwdStep& s, int D, hipStream_t st);

@@ -129,10 +129,19 @@ static int copy_block(const RingProblem& P, const void* src_all, char* dst, int 
   return RA_OK;
 }
 
-// Enqueue the whole ring: `launch(t, hosts_of_step)` is called once per step with, for
-// every active host, (host, block, kv pointers, batch stride, first/last flags).
+// Enqueue the whole ring: `launch(t, hosts_of_step, ..., forward)` is called once per step
+// with, for every active host, (host, block, kv pointers, batch stride, first/last flags).
+//
+// The block a host needs at step t+1 is the one its predecessor holds at step t.  In the
+// bf16 backward (`allow_forward`), when the call covers every host of the ring in ring
+// order, the step-t dK/dV kernel writes that block into the successor's receive slot
+// itself from the rows it loads anyway -- the send half of the ring's exchange, with no
+// separate copy.  Otherwise (the forward, whose step kernel has no registers to spare for
+// it; one host's share; a custom order; float32; or RINGATTN_SERIAL_COPY set) each step's
+// blocks are copied from their home rows into the receive slots by device-to-device
+// copies, on a side stream two steps ahead (or serially on the caller stream).
 template <class Launch>
-static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, char* recv_base,
+static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, char* recv_base, bool allow_forward,
                     Launch&& launch) {
   const int N = P.N;
   const int nh = (int)P.hosts.size();
@@ -152,8 +161,10 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
 
   const bool serial = env_flag("RINGATTN_SERIAL_COPY");
   const bool poison = env_flag("RINGATTN_POISON");
+  bool forward = allow_forward && N > 1 && !serial && P.elt == 2 && nh == N && P.order.empty();
+  for (int s = 0; forward && s < nh; ++s) forward = P.hosts[s] == s;
   hipStream_t side = stream;
-  if (!serial && N > 1) {
+  if (!serial && !forward && N > 1) {
     int rc = side_stream(&side);
     if (rc) return rc;
   }
@@ -184,7 +195,7 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
     }
     return RA_OK;
   };
-  if (N > 1 && !serial) {
+  if (N > 1 && !serial && !forward) {
     int rc = enqueue_copies(1);
     if (!rc && N > 2) rc = enqueue_copies(2);
     if (rc) return rc;
@@ -192,7 +203,7 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
 
   const size_t rowe = (size_t)P.H * P.D;
   for (int t = 0; t < N; ++t) {
-    if (t >= 1) {
+    if (t >= 1 && !forward) {
       if (serial) {
         int rc = enqueue_copies(t);
         if (rc) return rc;
@@ -223,9 +234,25 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
       host_ids.push_back(i);
       blk_ids.push_back(j);
     }
-    int rc = launch(t, hs, host_ids, blk_ids);
+    StepForward fw{};
+    for (int n = 0; n < kMaxSlots; ++n) fw.to[n] = -1;
+    if (forward && t + 1 < N) {
+      const int nxt = (t + 1) & 1;
+      fw.k0 = rb.k(nxt, 0);
+      fw.v0 = rb.v(nxt, 0);
+      fw.blk_bytes = (long long)rb.blk_bytes;
+      for (size_t n = 0; n < hs.size(); ++n) {
+        const int succ = (host_ids[n] + 1) % N;  // holds block blk_ids[n] at step t+1
+        if (P.active(succ, blk_ids[n])) fw.to[n] = (signed char)succ;
+      }
+      if (poison) {  // a receive slot the step-t kernels leave unwritten would read NaN
+        RA_HIP(hipMemsetAsync(rb.k(nxt, 0), 0xFF, rb.blk_bytes * nh, stream));
+        RA_HIP(hipMemsetAsync(rb.v(nxt, 0), 0xFF, rb.blk_bytes * nh, stream));
+      }
+    }
+    int rc = launch(t, hs, host_ids, blk_ids, fw);
     if (rc) return rc;
-    if (!serial && t >= 1 && t + 2 < N) {
+    if (!serial && !forward && t >= 1 && t + 2 < N) {
       hipEvent_t done;
       rc = R.event(&done);
       if (rc) return rc;
@@ -276,8 +303,8 @@ static int run_fwd(const RingProblem& P, void* o, float* lse, hipStream_t stream
   st.c = P.c();
   st.causal = P.causal;
   st.scale = 1.0f / sqrtf((float)P.D);
-  return run_ring(P, stream, R, base, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
-                                          const std::vector<int>&) -> int {
+  return run_ring(P, stream, R, base, false, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
+                                                 const std::vector<int>&, const StepForward&) -> int {
     st.n_slots = (int)hs.size();
     for (size_t s = 0; s < hs.size(); ++s) st.host[s] = hs[s];
     RA_HIP(timed_launch(RA_KERNEL_ATTN_FWD, stream, [&] {
@@ -331,9 +358,10 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
   st.c = P.c();
   st.causal = P.causal;
   st.scale = 1.0f / sqrtf((float)P.D);
-  rc = run_ring(P, stream, R, base, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
-                                        const std::vector<int>& blks) -> int {
+  rc = run_ring(P, stream, R, base, true, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
+                                              const std::vector<int>& blks, const StepForward& fw) -> int {
     st.n_slots = (int)hs.size();
+    st.fwd = fw;
     for (size_t s = 0; s < hs.size(); ++s) {
       st.host[s] = hs[s];
       st.dkv_row0[s] = blks[s] * P.c();

@@ -110,17 +110,26 @@ def test_bf16_one_host_share(host):
     assert max_err(lse, lse_ref) <= TOL_O
 
 
+@pytest.mark.parametrize("causal", [0, 1])
 @pytest.mark.parametrize("env", ["RINGATTN_SERIAL_COPY", "RINGATTN_POISON"])
-def test_bf16_copy_modes_match(env, monkeypatch):
-    """Receive buffers poisoned with NaN before every copy, or copies serialised on the
-    caller stream, give bit-identical results to the overlapped default."""
+def test_bf16_copy_modes_match(env, causal, monkeypatch):
+    """The key/value blocks reach every host's receive slot by side-stream copies (forward)
+    or by the backward step kernels forwarding the block they hold to the next host.
+    Receive slots poisoned with NaN before they are to be filled, or copies serialised on
+    the caller stream (which also replaces the backward's forwarding by copies), give
+    bit-identical forward and backward results to the default."""
     B, S, H, D, N = 1, 2048, 2, 128, 8
-    q, k, v = dev(*synth.attention_inputs(8, B, S, H, D))
-    o0, l0 = ra.attention_fwd(q, k, v, N, True)
+    q, k, v, do = dev(*synth.attention_inputs(8, B, S, H, D, with_grad=True))
+    o0, l0 = ra.attention_fwd(q, k, v, N, causal)
+    g0 = ra.attention_bwd(q, k, v, o0, l0, do, N, causal)
     monkeypatch.setenv(env, "1")
-    o1, l1 = ra.attention_fwd(q, k, v, N, True)
+    o1, l1 = ra.attention_fwd(q, k, v, N, causal)
+    g1 = ra.attention_bwd(q, k, v, o0, l0, do, N, causal)
     torch.cuda.synchronize()
     assert torch.equal(o0, o1) and torch.equal(l0, l1)
+    for a, b in zip(g0, g1):
+        assert torch.equal(a, b)
+        assert not torch.isnan(a.float()).any()
 
 
 @pytest.mark.parametrize("N", [1, 2, 8])

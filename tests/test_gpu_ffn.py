@@ -77,9 +77,14 @@ def test_blockwise_ffn_block_size_invariance():
     assert torch.equal(y1, y2)
 
 
-def test_blockwise_linear_forward_backward():
-    T, di, do, blk = 512, 512, 256, 256
-    g = torch.Generator().manual_seed(50)
+# The GEMM walks K in steps of 32 through a five-stage ring, in groups of five steps plus a
+# remainder of 0..4 steps: K = 512 (16 steps), 768 (24), 1280 (40) and 256 (8) cover
+# remainders 1, 4, 0 and 3 across the forward (K = d_in), dX (K = d_out) and dW (K = block)
+# products.
+@pytest.mark.parametrize("T,di,do,blk", [(512, 512, 256, 256), (512, 768, 1280, 256), (768, 1280, 768, 768)])
+def test_blockwise_linear_forward_backward(T, di, do, blk):
+    log("linear T=%d d_in=%d d_out=%d block=%d" % (T, di, do, blk))
+    g = torch.Generator().manual_seed(50 + di)
     x = torch.randn(T, di, generator=g).to(torch.bfloat16)
     w = (torch.randn(di, do, generator=g) * 0.02).to(torch.bfloat16)
     r = torch.randn(T, do, generator=g).to(torch.bfloat16)
