@@ -122,6 +122,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   const int b = bh / p.H, h = bh % p.H;
   const StepHost hs = p.host[slot];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // uniform: LDS destinations in scalar registers
   const int rs = p.H * D;
   const float sl2 = p.scale * kLog2e;
 
@@ -131,10 +132,10 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   const bf16* vrow = (const bf16*)hs.v + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
   // forwarding: the workgroup writes the rows of its 128 keys, as loaded, into the next
   // host's receive slot for the next ring step (layout [B, c, H, D])
-  const int fto = p.fwd.to[slot];
+  const int fto = p.fwd.to[slot] - 1;  // destination slot, or -1
   bf16* fkrow = nullptr;
   bf16* fvrow = nullptr;
-  if (fto >= 0) {
+  if (fto >= 0 && p.fwd.k0 != nullptr && p.fwd.v0 != nullptr) {
     const long long off = (long long)fto * p.fwd.blk_bytes + 2 * (((long long)b * p.c + key_in_blk) * rs + h * D);
     fkrow = (bf16*)((char*)p.fwd.k0 + off);
     fvrow = (bf16*)((char*)p.fwd.v0 + off);
@@ -184,13 +185,13 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     const long long t0 = (long long)(hs.q_row0 + qt * kQB) * rs;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      buffer_load_lds16(qbase + t0, kQB * rs * 2, pick(Bc, sQ0, sQ1, sQ2) + (wave * RPW + j * ROWS_PER_LOAD) * D,
+      buffer_load_lds16(qbase + t0, kQB * rs * 2, pick(Bc, sQ0, sQ1, sQ2) + (wave_u * RPW + j * ROWS_PER_LOAD) * D,
                         goff[j]);
-      buffer_load_lds16(obase + t0, kQB * rs * 2, pick(Bc, sO0, sO1, sO2) + (wave * RPW + j * ROWS_PER_LOAD) * D,
+      buffer_load_lds16(obase + t0, kQB * rs * 2, pick(Bc, sO0, sO1, sO2) + (wave_u * RPW + j * ROWS_PER_LOAD) * D,
                         goff[j]);
     }
-    if (wave == 0) buffer_load_lds4(p.lse + lrow0 + qt * kQB, kQB * 4, pick(Bc, sL0, sL1, sL2), 4 * lane);
-    if (wave == 1) buffer_load_lds4(p.delta + lrow0 + qt * kQB, kQB * 4, pick(Bc, sD0, sD1, sD2), 4 * lane);
+    if (wave_u == 0) buffer_load_lds4(p.lse + lrow0 + qt * kQB, kQB * 4, pick(Bc, sL0, sL1, sL2), 4 * lane);
+    if (wave_u == 1) buffer_load_lds4(p.delta + lrow0 + qt * kQB, kQB * 4, pick(Bc, sD0, sD1, sD2), 4 * lane);
   };
   const int qrow = swap_bits23(l32);
   int roff[NKK];
@@ -442,6 +443,7 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   const int b = bh / p.H, h = bh % p.H;
   const StepHost hs = p.host[slot];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // uniform: LDS destinations in scalar registers
   const int rs = p.H * D;
 
   const int qr = hs.q_row0 + qt * kQQ + wave * 32 + l32;
@@ -491,8 +493,8 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
     const long long t0 = (long long)it * kKK * rs;
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      buffer_load_lds16(kbase + t0, kKK * rs * 2, pick(Bc, sK0, sK1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
-      buffer_load_lds16(vbase + t0, kKK * rs * 2, pick(Bc, sV0, sV1) + (wave * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16(kbase + t0, kKK * rs * 2, pick(Bc, sK0, sK1) + (wave_u * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16(vbase + t0, kKK * rs * 2, pick(Bc, sV0, sV1) + (wave_u * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
     }
   };
   // row reads (A operand, rows 32 mt + swap_bits23(l32)) and transpose reads of the tiles
@@ -772,6 +774,10 @@ hipError_t launch_bwd_pre_f32(const float* o, const float* dO, float* delta, int
 
 hipError_t launch_bwd_bf16(const BwdStep& s, int D, hipStream_t st) {
   if (s.n_slots == 0) return hipSuccess;
+  // a forwarding destination needs both receive bases and a slot size
+  for (int n = 0; n < s.n_slots; ++n)
+    if (s.fwd.to[n] != 0 && (s.fwd.to[n] < 0 || s.fwd.k0 == nullptr || s.fwd.v0 == nullptr || s.fwd.blk_bytes <= 0))
+      return hipErrorInvalidValue;
   const int g1 = s.n_slots * s.B * s.H * (s.c / kKB);
   const int g2 = s.n_slots * s.B * s.H * (s.c / kQQ);
   if (D == 128) {

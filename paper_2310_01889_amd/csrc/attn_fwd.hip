@@ -80,6 +80,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   const StepHost hs = p.host[slot];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // uniform: LDS destinations in scalar registers
   const int l32 = lane & 31, hi = lane >> 5;
   const int rs = p.H * D;  // row stride of q / k / v / o (elements)
 
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   auto dload = [&](const bf16* src_tile, bf16* dst_tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j)
-      buffer_load_lds16(src_tile, kBN * rs * 2, dst_tile + (wave * RPW + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16(src_tile, kBN * rs * 2, dst_tile + (wave_u * RPW + j * ROWS_PER_LOAD) * D, goff[j]);
   };
   auto load_k = [&](int it, auto Bc) __attribute__((always_inline)) { dload(kbase + (long long)it * kBN * rs, kbuf(Bc)); };
   auto load_v = [&](int it, auto Bc) __attribute__((always_inline)) { dload(vbase + (long long)it * kBN * rs, vbuf(Bc)); };

@@ -16,7 +16,8 @@ constexpr int kLast = 2;             // host's last active step: finalize o = ac
 // t+1).  The bf16 backward step kernels copy the block's rows, while they have them in
 // hand, into that host's receive slot for the next step: slot s of the next step's half of
 // the receive buffers starts at k0 + s * blk_bytes (v0 for values), in the layout
-// [B, c, H, D].  to[n] is the destination slot of launch slot n, or -1 (no forwarding).
+// [B, c, H, D].  to[n] is 1 + the destination slot of launch slot n, or 0 for none, so
+// that a zero-initialised descriptor forwards nothing.
 struct StepForward {
   const void* k0;
   const void* v0;

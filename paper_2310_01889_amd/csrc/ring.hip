@@ -234,8 +234,7 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
       host_ids.push_back(i);
       blk_ids.push_back(j);
     }
-    StepForward fw{};
-    for (int n = 0; n < kMaxSlots; ++n) fw.to[n] = -1;
+    StepForward fw{};  // zero: no forwarding
     if (forward && t + 1 < N) {
       const int nxt = (t + 1) & 1;
       fw.k0 = rb.k(nxt, 0);
@@ -243,7 +242,7 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
       fw.blk_bytes = (long long)rb.blk_bytes;
       for (size_t n = 0; n < hs.size(); ++n) {
         const int succ = (host_ids[n] + 1) % N;  // holds block blk_ids[n] at step t+1
-        if (P.active(succ, blk_ids[n])) fw.to[n] = (signed char)succ;
+        if (P.active(succ, blk_ids[n])) fw.to[n] = (signed char)(succ + 1);
       }
       if (poison) {  // a receive slot the step-t kernels leave unwritten would read NaN
         RA_HIP(hipMemsetAsync(rb.k(nxt, 0), 0xFF, rb.blk_bytes * nh, stream));
