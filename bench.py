@@ -12,7 +12,10 @@ the timed region.  Prints ONE JSON line.
 `value` is TFLOP/s of algorithmic work (4*B*H*D per visible (query, key) pair; causal
 masking halves the diagonal blocks and skips blocks above the diagonal).  The
 `roofline` object reports the step kernel's own throughput (HIP events around every
-launch, on the stream it runs on) against the bf16 dense matrix-core peak.  The
+launch, on the stream it runs on) against the bf16 dense matrix-core peak, and beside it
+against the rate the chip sustains on back-to-back matrix products alone (the library's
+calibration kernel, measured in the same run).  `ms_per_step` is the mean over the timed
+calls, with their median and minimum alongside.  The
 `cpu_baseline` object times the fp64 CPU oracle on one head of the same workload and
 scales it to all 32 heads.  `extra` holds secondary configurations measured in the same
 run (forward+backward at S=16384, one host's share at 262144 tokens, ring decode of 1 and 8
@@ -58,6 +61,52 @@ def time_calls(fn, steps, warmup):
     return e0.elapsed_time(e1) / steps, wall
 
 
+def time_calls_each(fn, steps):
+    """Times `steps` back-to-back calls with an event between consecutive calls: returns
+    (mean, median, min) milliseconds per call and the host wall time."""
+    import statistics
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for i in range(steps):
+        fn()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return sum(per) / steps, statistics.median(per), min(per), wall
+
+
+def mfma_loop_peak(ra, torch, iters=3000, reps=5):
+    """Matrix-core throughput the chip sustains with nothing else running (the library's
+    calibration kernel: 2048 waves of independent bf16 32x32x16 product chains), TFLOP/s,
+    median of `reps` timed launches."""
+    import statistics
+    for _ in range(2):
+        ra.mfma_probe(iters)
+    torch.cuda.synchronize()
+    rates = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fl = ra.mfma_probe(iters)
+        e1.record()
+        torch.cuda.synchronize()
+        rates.append(fl / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+    return statistics.median(rates)
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(B, S, H, D):
     """fp64 oracle on one head of the workload, scaled to all heads."""
     import numpy as np
@@ -74,6 +123,7 @@ def cpu_baseline(B, S, H, D):
         "value": flops_one_head / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": "oracle.attention.attention_fwd (fp64, NumPy BLAS) on 1 of %d heads of the "
                   "workload (B=%d, S=%d, D=%d, causal): %.1f s; whole workload extrapolated "
@@ -246,13 +296,14 @@ def main():
     torch.cuda.synchronize()
     ra.timing_read(ra.KERNEL_ATTN_FWD)
     ra.timing_enable(True)
-    ms, wall = time_calls(step, args.steps, 0)
+    ms, ms_med, ms_min, wall = time_calls_each(step, args.steps)
     ra.timing_enable(False)
     kms, launches = ra.timing_read(ra.KERNEL_ATTN_FWD)
     k_avg_ms = kms / max(1, launches)
     flops_per_launch = flops / N  # N launches per step
     achieved = flops_per_launch / (k_avg_ms * 1e-3) / 1e12
     value = flops / (ms * 1e-3) / 1e12
+    mfma_loop = mfma_loop_peak(ra, torch)
 
     out = {
         "metric": METRIC,
@@ -262,6 +313,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_median": round(ms_med, 4),
+        "ms_per_step_min": round(ms_min, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -275,7 +328,9 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (attention step)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
-                     "avg_launch_ms": round(k_avg_ms, 4), "launches": launches},
+                     "avg_launch_ms": round(k_avg_ms, 4), "launches": launches,
+                     "mfma_loop_measured": round(mfma_loop, 1),
+                     "frac_of_mfma_loop": round(achieved / mfma_loop, 4)},
     }
 
     if not args.no_extra:

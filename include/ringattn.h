@@ -325,6 +325,17 @@ enum { RA_KERNEL_ATTN_FWD = 0, RA_KERNEL_ATTN_BWD = 1, RA_KERNEL_GEMM = 2, RA_KE
 void ring_attn_timing_enable(int on);
 int ring_attn_timing_read(int kind, double* total_ms, int* launches);
 
+/*
+ * Matrix-core calibration for benchmarks (not part of the method): launches 512
+ * workgroups of 256 threads (two waves per SIMD on 256 compute units); every wave issues
+ * iters x 32 bf16 32x32x16 matrix products (4 independent accumulator chains) and writes
+ * one float to sink[wave].  The caller times the launch on `stream`: the work is
+ * 2048 * iters * 32 * 32768 flop.
+ *   iters  in [1, 2^20] (else RA_EINVAL)
+ *   sink   device float[2048], overwritten
+ */
+int ring_attn_mfma_probe(int iters, float* sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -34,6 +34,7 @@ _LIB = None
 _P = ctypes.c_void_p
 _I = ctypes.c_int
 _SIGS = {
+    "ring_attn_mfma_probe": [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p],
     "ring_attn_fwd": [_P] * 5 + [_I] * 6 + [_P],
     "ring_attn_fwd_f32": [_P] * 5 + [_I] * 6 + [_P],
     "ring_attn_bwd": [_P] * 9 + [_I] * 6 + [_P],
@@ -119,6 +120,18 @@ def timing_read(kind):
     if rc != 0:
         raise RingAttnError("ring_attn_timing_read", rc, lib.ring_attn_last_error().decode())
     return ms.value, n.value
+
+
+MFMA_PROBE_WAVES = 2048
+
+
+def mfma_probe(iters, stream=None):
+    """Launch the matrix-core calibration kernel (ring_attn_mfma_probe) on the current
+    stream; returns the flops it performs.  Time it with events around the call."""
+    import torch
+    sink = torch.empty(MFMA_PROBE_WAVES, dtype=torch.float32, device="cuda")
+    _call("ring_attn_mfma_probe", int(iters), sink.data_ptr(), _stream(stream))
+    return float(MFMA_PROBE_WAVES) * iters * 32 * 32768
 
 
 def _call(name, *args):

@@ -126,3 +126,10 @@ def test_product_path_does_not_use_the_oracle():
             if f.endswith((".py", ".hip", ".h", ".cpp")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"^\s*(from|import)\s+oracle\b", text, flags=re.M), f
+
+
+def test_mfma_probe_argument_validation(lib):
+    assert lib.ring_attn_mfma_probe(1, NULL, NULL) == RA_EINVAL
+    assert lib.ring_attn_mfma_probe(0, FAKE, NULL) == RA_EINVAL
+    assert lib.ring_attn_mfma_probe((1 << 20) + 1, FAKE, NULL) == RA_EINVAL
+    assert b"iters" in lib.ring_attn_last_error()
