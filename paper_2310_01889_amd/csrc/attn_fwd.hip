@@ -456,6 +456,32 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       p.l[st_row] = l_tot;
     }
   }
+
+  // ---- send: rows 128 qt .. 128 qt + 127 of (b, h) of this host's block to the host
+  // that needs the block at the next step (the ring's exchange, done by the workgroups
+  // as they finish instead of by copies between the steps)
+  const int fto = p.fwd.to[slot] - 1;  // destination slot, or -1
+  if (fto >= 0 && p.fwd.k0 != nullptr && p.fwd.v0 != nullptr) {
+    constexpr int PER = kBM * CPR / kThreads;  // 16-byte chunks per thread per operand
+    const long long doff = (long long)fto * p.fwd.blk_bytes + 2 * ((long long)b * p.c * rs + h * D);
+    bf16* kdst = (bf16*)((char*)p.fwd.k0 + doff);
+    bf16* vdst = (bf16*)((char*)p.fwd.v0 + doff);
+    u32x4 kx[PER], vx[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int idx = e * kThreads + tid;
+      const long long off = (long long)(qt * kBM + idx / CPR) * rs + 8 * (idx % CPR);
+      kx[e] = *(const u32x4*)(kbase + off);
+      vx[e] = *(const u32x4*)(vbase + off);
+    }
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int idx = e * kThreads + tid;
+      const long long off = (long long)(qt * kBM + idx / CPR) * rs + 8 * (idx % CPR);
+      *(u32x4*)(kdst + off) = kx[e];
+      *(u32x4*)(vdst + off) = vx[e];
+    }
+  }
 }
 
 // ===================================================================================
@@ -562,6 +588,10 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(const FwdStep p) {
 hipError_t launch_fwd_bf16(const FwdStep& s, int D, hipStream_t st) {
   const int total = s.n_slots * s.B * s.H * (s.c / kBM);
   if (total == 0) return hipSuccess;
+  // a forwarding destination needs both receive bases and a slot size
+  for (int n = 0; n < s.n_slots; ++n)
+    if (s.fwd.to[n] != 0 && (s.fwd.to[n] < 0 || s.fwd.k0 == nullptr || s.fwd.v0 == nullptr || s.fwd.blk_bytes <= 0))
+      return hipErrorInvalidValue;
   if (D == 128)
     hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(total), dim3(kThreads), 0, st, s);
   else

@@ -13,8 +13,9 @@ constexpr int kLast = 2;             // host's last active step: finalize o = ac
 
 // Forwarding of the key/value block a host holds to the host that needs it at the next
 // ring step (host i at step t holds block j = (i - t) mod N, which host i+1 holds at step
-// t+1).  The bf16 backward step kernels copy the block's rows, while they have them in
-// hand, into that host's receive slot for the next step: slot s of the next step's half of
+// t+1).  The bf16 step kernels copy the block's rows into that host's receive slot for the
+// next step (the backward's dK/dV kernel from the rows it has in hand; the forward kernel
+// after its own work, each workgroup its 128-row slice): slot s of the next step's half of
 // the receive buffers starts at k0 + s * blk_bytes (v0 for values), in the layout
 // [B, c, H, D].  to[n] is 1 + the destination slot of launch slot n, or 0 for none, so
 // that a zero-initialised descriptor forwards nothing.
@@ -48,6 +49,7 @@ struct FwdStep {
   long long q_bstride;    // Sq * H * D
   int n_slots, B, H, Sq, c, causal;
   float scale;            // 1 / sqrt(D)
+  StepForward fwd;        // bf16 kernel only: forward each slot's block to the next host
 };
 
 // Backward step: one key/value block per host; dq accumulates per host, dk/dv per block.

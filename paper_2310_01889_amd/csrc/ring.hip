@@ -72,7 +72,7 @@ int side_stream(hipStream_t* out) {
 namespace {
 std::mutex g_tmu;
 bool g_timing = false;
-struct TimedLaunch { int kind; hipEvent_t a, b; };
+struct TimedLaunch { int kind; hipEvent_t a, b; bool own_a; };
 std::vector<TimedLaunch> g_timed;
 }  // namespace
 
@@ -81,9 +81,9 @@ bool timing_on() {
   return g_timing;
 }
 
-void timing_push(int kind, hipEvent_t a, hipEvent_t b) {
+void timing_push(int kind, hipEvent_t a, hipEvent_t b, bool own_a) {
   std::lock_guard<std::mutex> lk(g_tmu);
-  g_timed.push_back({kind, a, b});
+  g_timed.push_back({kind, a, b, own_a});
 }
 
 static bool env_flag(const char* name) {
@@ -129,20 +129,20 @@ static int copy_block(const RingProblem& P, const void* src_all, char* dst, int 
   return RA_OK;
 }
 
-// Enqueue the whole ring: `launch(t, hosts_of_step, ..., forward)` is called once per step
-// with, for every active host, (host, block, kv pointers, batch stride, first/last flags).
+// Enqueue the whole ring: `launch(t, hosts_of_step, ..., forward, contiguous)` is called once
+// per step with, for every active host, (host, block, kv pointers, batch stride, first/last
+// flags); `contiguous` says that nothing was enqueued on the stream since the previous step.
 //
-// The block a host needs at step t+1 is the one its predecessor holds at step t.  In the
-// bf16 backward (`allow_forward`), when the call covers every host of the ring in ring
-// order, the step-t dK/dV kernel writes that block into the successor's receive slot
-// itself from the rows it loads anyway -- the send half of the ring's exchange, with no
-// separate copy.  Otherwise (the forward, whose step kernel has no registers to spare for
-// it; one host's share; a custom order; float32; or RINGATTN_SERIAL_COPY set) each step's
+// The block a host needs at step t+1 is the one its predecessor holds at step t.  In bf16,
+// when the call covers every host of the ring in ring order, the step-t kernels write that
+// block into the successor's receive slot themselves (the forward kernel's workgroups as
+// they finish, the backward's dK/dV kernel from the rows it loads anyway) -- the send half
+// of the ring's exchange, with no separate copy and no wait between the steps.  Otherwise
+// (one host's share; a custom order; float32; or RINGATTN_SERIAL_COPY set) each step's
 // blocks are copied from their home rows into the receive slots by device-to-device
 // copies, on a side stream two steps ahead (or serially on the caller stream).
 template <class Launch>
-static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, char* recv_base, bool allow_forward,
-                    Launch&& launch) {
+static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, char* recv_base, Launch&& launch) {
   const int N = P.N;
   const int nh = (int)P.hosts.size();
   RecvBuffers rb;
@@ -161,7 +161,7 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
 
   const bool serial = env_flag("RINGATTN_SERIAL_COPY");
   const bool poison = env_flag("RINGATTN_POISON");
-  bool forward = allow_forward && N > 1 && !serial && P.elt == 2 && nh == N && P.order.empty();
+  bool forward = N > 1 && !serial && P.elt == 2 && nh == N && P.order.empty();
   for (int s = 0; forward && s < nh; ++s) forward = P.hosts[s] == s;
   hipStream_t side = stream;
   if (!serial && !forward && N > 1) {
@@ -249,7 +249,9 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
         RA_HIP(hipMemsetAsync(rb.v(nxt, 0), 0xFF, rb.blk_bytes * nh, stream));
       }
     }
-    int rc = launch(t, hs, host_ids, blk_ids, fw);
+    // contiguous: nothing has been enqueued on the stream since the previous step's launch
+    const bool contiguous = t > 0 && forward && !poison;
+    int rc = launch(t, hs, host_ids, blk_ids, fw, contiguous);
     if (rc) return rc;
     if (!serial && !forward && t >= 1 && t + 2 < N) {
       hipEvent_t done;
@@ -302,13 +304,16 @@ static int run_fwd(const RingProblem& P, void* o, float* lse, hipStream_t stream
   st.c = P.c();
   st.causal = P.causal;
   st.scale = 1.0f / sqrtf((float)P.D);
-  return run_ring(P, stream, R, base, false, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
-                                                 const std::vector<int>&, const StepForward&) -> int {
+  hipEvent_t chain = nullptr;  // end event of the previous step's launch (timing)
+  return run_ring(P, stream, R, base, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
+                                         const std::vector<int>&, const StepForward& fw, bool contiguous) -> int {
     st.n_slots = (int)hs.size();
     for (size_t s = 0; s < hs.size(); ++s) st.host[s] = hs[s];
+    st.fwd = fw;
+    if (!contiguous) chain = nullptr;
     RA_HIP(timed_launch(RA_KERNEL_ATTN_FWD, stream, [&] {
       return P.elt == 2 ? launch_fwd_bf16(st, P.D, stream) : launch_fwd_f32(st, P.D, stream);
-    }));
+    }, &chain));
     return RA_OK;
   });
 }
@@ -357,17 +362,19 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
   st.c = P.c();
   st.causal = P.causal;
   st.scale = 1.0f / sqrtf((float)P.D);
-  rc = run_ring(P, stream, R, base, true, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
-                                              const std::vector<int>& blks, const StepForward& fw) -> int {
+  hipEvent_t chain = nullptr;  // end event of the previous step's launch (timing)
+  rc = run_ring(P, stream, R, base, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
+                                       const std::vector<int>& blks, const StepForward& fw, bool contiguous) -> int {
     st.n_slots = (int)hs.size();
     st.fwd = fw;
     for (size_t s = 0; s < hs.size(); ++s) {
       st.host[s] = hs[s];
       st.dkv_row0[s] = blks[s] * P.c();
     }
+    if (!contiguous) chain = nullptr;
     RA_HIP(timed_launch(RA_KERNEL_ATTN_BWD, stream, [&] {
       return f32 ? launch_bwd_f32(st, P.D, stream) : launch_bwd_bf16(st, P.D, stream);
-    }));
+    }, &chain));
     return RA_OK;
   });
   if (rc) return rc;
@@ -563,7 +570,11 @@ int ring_attn_timing_read(int kind, double* total_ms, int* launches) {
       if (e != hipSuccess) rc = set_err(RA_EHIP, "timing event: %s", hipGetErrorString(e));
     }
     sum += ms;
-    (void)hipEventDestroy(t.a);
+  }
+  // an entry's start event may be the end event of the entry before it: destroy once all
+  // durations are read
+  for (const TimedLaunch& t : mine) {
+    if (t.own_a) (void)hipEventDestroy(t.a);
     (void)hipEventDestroy(t.b);
   }
   *total_ms = sum;

@@ -198,3 +198,32 @@ def test_errors_leave_outputs_untouched():
     assert e.value.code == 2
     torch.cuda.synchronize()
     assert bool((o == 7.0).all()) and bool((lse == 7.0).all())
+
+
+@pytest.mark.parametrize("n_hosts", [8, 1])
+def test_launch_timing_counts_and_bounds(n_hosts):
+    """ring_attn_timing_*: one timed entry per ring step (consecutive steps share their
+    boundary event), durations positive and together within the call's own duration."""
+    log("timing case n_hosts=%d" % n_hosts)
+    q, k, v = dev(*synth.attention_inputs(5, 1, 2048, 2, 128, torch.bfloat16))
+    o, lse = ra.attention_fwd(q, k, v, n_hosts, True)  # warm-up
+    dO = torch.ones_like(q)
+    torch.cuda.synchronize()
+    for kind in (ra.KERNEL_ATTN_FWD, ra.KERNEL_ATTN_BWD):
+        ra.timing_read(kind)
+    ra.timing_enable(True)
+    try:
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record()
+        o, lse = ra.attention_fwd(q, k, v, n_hosts, True)
+        e[1].record()
+        ra.attention_bwd(q, k, v, o, lse, dO, n_hosts, True)
+        e[2].record()
+        torch.cuda.synchronize()
+    finally:
+        ra.timing_enable(False)
+    for kind, i in ((ra.KERNEL_ATTN_FWD, 0), (ra.KERNEL_ATTN_BWD, 1)):
+        ms, n = ra.timing_read(kind)
+        assert n == n_hosts
+        assert 0 < ms <= e[i].elapsed_time(e[i + 1]) * 1.01 + 0.01
+        assert ra.timing_read(kind) == (0.0, 0)
