@@ -387,8 +387,10 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     if (ql < qt_free) last(std::true_type{}); else last(std::false_type{});
   }
 
-  // add into the float32 gradient of the block (its home rows); dK carries the 1/sqrt(D)
+  // add into the float32 gradient of the block (its home rows); dK carries the 1/sqrt(D).
+  // The block's first contribution is written, not added; its last goes out in bf16.
   const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key_in_blk) * rs + h * D;
+  const int kf = p.dkv_flags[slot];
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -396,14 +398,23 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       const int d = 32 * dt + 8 * gg + 4 * hi;
       f32x4* dkp = (f32x4*)(p.dk + grow + d);
       f32x4* dvp = (f32x4*)(p.dv + grow + d);
-      f32x4 k4 = *dkp, v4 = *dvp;
+      f32x4 k4 = {0.f, 0.f, 0.f, 0.f}, v4 = {0.f, 0.f, 0.f, 0.f};
+      if (!(kf & kFirst)) {
+        k4 = *dkp;
+        v4 = *dvp;
+      }
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         k4[e] += dkacc[dt][4 * gg + e] * p.scale;
         v4[e] += dvacc[dt][4 * gg + e];
       }
-      *dkp = k4;
-      *dvp = v4;
+      if (kf & kLast) {
+        *(u32x2*)((bf16*)p.dk_out + grow + d) = u32x2{pack_bf16x2(k4[0], k4[1]), pack_bf16x2(k4[2], k4[3])};
+        *(u32x2*)((bf16*)p.dv_out + grow + d) = u32x2{pack_bf16x2(v4[0], v4[1]), pack_bf16x2(v4[2], v4[3])};
+      } else {
+        *dkp = k4;
+        *dvp = v4;
+      }
     }
 }
 
@@ -582,18 +593,26 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   run(std::false_type{}, 0, n_full);
   run(std::true_type{}, n_full, nt);
 
-  // dq (float32, [B, Sq, H, D]) += scale * dQ
-  float* dqrow = p.dq + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+  // dq (float32, [B, Sq, H, D]) += scale * dQ; with dq_out set, the host's first active
+  // step writes instead of adding and its last writes the bf16 result
+  const long long qoff = (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+  float* dqrow = p.dq + qoff;
+  const bool first = p.dq_out != nullptr && (hs.flags & kFirst);
+  const bool fin = p.dq_out != nullptr && (hs.flags & kLast);
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
     for (int gg = 0; gg < 4; ++gg) {
       const int d = 32 * dt + 8 * gg + 4 * hi;
       f32x4* dp = (f32x4*)(dqrow + d);
-      f32x4 t = *dp;
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+      if (!first) t = *dp;
 #pragma unroll
       for (int e = 0; e < 4; ++e) t[e] += dqacc[dt][4 * gg + e] * p.scale;
-      *dp = t;
+      if (fin)
+        *(u32x2*)((bf16*)p.dq_out + qoff + d) = u32x2{pack_bf16x2(t[0], t[1]), pack_bf16x2(t[2], t[3])};
+      else
+        *dp = t;
     }
 }
 
@@ -778,6 +797,9 @@ hipError_t launch_bwd_bf16(const BwdStep& s, int D, hipStream_t st) {
   for (int n = 0; n < s.n_slots; ++n)
     if (s.fwd.to[n] != 0 && (s.fwd.to[n] < 0 || s.fwd.k0 == nullptr || s.fwd.v0 == nullptr || s.fwd.blk_bytes <= 0))
       return hipErrorInvalidValue;
+  // a last touch needs the bf16 outputs
+  for (int n = 0; n < s.n_slots; ++n)
+    if ((s.dkv_flags[n] & kLast) && (s.dk_out == nullptr || s.dv_out == nullptr)) return hipErrorInvalidValue;
   const int g1 = s.n_slots * s.B * s.H * (s.c / kKB);
   const int g2 = s.n_slots * s.B * s.H * (s.c / kQQ);
   if (D == 128) {

@@ -69,6 +69,15 @@ struct BwdStep {
   float scale;
   StepForward fwd;        // bf16 dK/dV kernel only: forward each slot's block (the keys a
                           // workgroup holds) to the next host
+  // bf16 kernels, when the call holds every contribution to the gradients: the block a slot
+  // holds is touched for the first time (kFirst: write dk / dv instead of adding into them)
+  // or the last time (kLast: write the final sum, rounded, to dk_out / dv_out instead).
+  // 0 = add into dk / dv.
+  unsigned char dkv_flags[kMaxSlots];
+  void* dk_out;           // bf16 [B, Skv, H, D] results (rows at the block's home position)
+  void* dv_out;
+  void* dq_out;           // bf16 [B, Sq, H, D]; when set, dq follows the host's kFirst / kLast
+                          // flags the same way (null: always add into dq)
 };
 
 hipError_t launch_fwd_bf16(const FwdStep& s, int D, hipStream_t st);

@@ -338,9 +338,23 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
   float* gq = f32 ? (float*)dq : lse2 + nrow;
   float* gk = f32 ? (float*)dk : gq + telems;
   float* gv = f32 ? (float*)dv : gk + telems;
-  RA_HIP(launch_zero_f32(gq, (long long)telems, stream));
-  RA_HIP(launch_zero_f32(gk, (long long)telems, stream));
-  RA_HIP(launch_zero_f32(gv, (long long)telems, stream));
+  // bf16: the call covers every host, so it holds every contribution to each gradient
+  // row: the first one is written and the last one goes out in bf16 (no zero fill, no
+  // cast).  float32: the outputs are zeroed and accumulated into.
+  std::vector<int> blk_first(P.N, -1), blk_last(P.N, -1);  // steps that touch block j
+  if (f32) {
+    RA_HIP(launch_zero_f32(gq, (long long)telems, stream));
+    RA_HIP(launch_zero_f32(gk, (long long)telems, stream));
+    RA_HIP(launch_zero_f32(gv, (long long)telems, stream));
+  } else {
+    for (int t = 0; t < P.N; ++t)
+      for (int i : P.hosts) {
+        const int j = P.blk(i, t);
+        if (!P.active(i, j)) continue;
+        if (blk_first[j] < 0) blk_first[j] = t;
+        blk_last[j] = t;
+      }
+  }
   if (f32)
     RA_HIP(launch_bwd_pre_f32((const float*)o, (const float*)dO, delta, P.B, P.Sq, P.H, P.D, stream));
   else
@@ -362,14 +376,22 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
   st.c = P.c();
   st.causal = P.causal;
   st.scale = 1.0f / sqrtf((float)P.D);
+  if (!f32) {
+    st.dq_out = dq;
+    st.dk_out = dk;
+    st.dv_out = dv;
+  }
   hipEvent_t chain = nullptr;  // end event of the previous step's launch (timing)
-  rc = run_ring(P, stream, R, base, [&](int, const std::vector<StepHost>& hs, const std::vector<int>&,
+  rc = run_ring(P, stream, R, base, [&](int t, const std::vector<StepHost>& hs, const std::vector<int>&,
                                        const std::vector<int>& blks, const StepForward& fw, bool contiguous) -> int {
     st.n_slots = (int)hs.size();
     st.fwd = fw;
     for (size_t s = 0; s < hs.size(); ++s) {
       st.host[s] = hs[s];
       st.dkv_row0[s] = blks[s] * P.c();
+      st.dkv_flags[s] = f32 ? 0
+                            : (unsigned char)((t == blk_first[blks[s]] ? kFirst : 0) |
+                                              (t == blk_last[blks[s]] ? kLast : 0));
     }
     if (!contiguous) chain = nullptr;
     RA_HIP(timed_launch(RA_KERNEL_ATTN_BWD, stream, [&] {
@@ -377,13 +399,7 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
     }, &chain));
     return RA_OK;
   });
-  if (rc) return rc;
-  if (!f32) {
-    RA_HIP(launch_cast_f32_bf16(gq, dq, (long long)telems, stream));
-    RA_HIP(launch_cast_f32_bf16(gk, dk, (long long)telems, stream));
-    RA_HIP(launch_cast_f32_bf16(gv, dv, (long long)telems, stream));
-  }
-  return RA_OK;
+  return rc;
 }
 
 // ---------------------------------------------------------------------------------
