@@ -424,7 +424,8 @@ static int run_bwd_host(const void* q_blk, const void* k_all, const void* v_all,
   const size_t blk = (size_t)c * rowe;         // elements of one block (per batch)
   const size_t nrow = (size_t)B * H * c;
   const size_t qel = (size_t)B * blk;
-  // workspace: K/V slots (bf16) and dK/dV slots (float32), 2 each; Delta, lse2; dq (float32)
+  // workspace: K/V slots (bf16) and dK/dV slots (float32), 2 each; Delta, lse2; dq (float32,
+  // written by the host's first active step, rounded into dq_blk by its last)
   const size_t kv_slot = qel * 2, g_slot = qel * 4;
   CallResources R(stream);
   int rc = R.alloc(4 * kv_slot + 4 * g_slot + 2 * nrow * 4 + qel * 4);
@@ -437,11 +438,13 @@ static int run_bwd_host(const void* q_blk, const void* k_all, const void* v_all,
   float* delta = (float*)(base + 4 * kv_slot + 4 * g_slot);
   float* lse2 = delta + nrow;
   float* dq32 = lse2 + nrow;
-  RA_HIP(launch_zero_f32(dq32, (long long)qel, stream));
   RA_HIP(launch_bwd_pre_bf16(o_blk, dO_blk, lse_blk, delta, lse2, B, c, H, D, stream));
 
   auto blk_of = [&](int t) { return ((host - t) % N + N) % N; };
   auto active = [&](int t) { return !causal || blk_of(t) <= host; };
+  int t_last = 0;  // the host's last active step (step 0, its own block, is always active)
+  for (int t = 0; t < N; ++t)
+    if (active(t)) t_last = t;
   hipStream_t side = stream;
   rc = side_stream(&side);
   if (rc) return rc;
@@ -480,6 +483,7 @@ static int run_bwd_host(const void* q_blk, const void* k_all, const void* v_all,
   st.lse = lse2;
   st.delta = delta;
   st.dq = dq32;
+  st.dq_out = dq_blk;
   st.q_bstride = (long long)blk;
   st.B = B;
   st.H = H;
@@ -512,6 +516,7 @@ static int run_bwd_host(const void* q_blk, const void* k_all, const void* v_all,
     h.q_row0 = 0;
     h.q_pos0 = host * c;
     h.k_pos0 = j * c;
+    h.flags = (t == 0 ? kFirst : 0) | (t == t_last ? kLast : 0);
     st.dkv_row0[0] = 0;
     RA_HIP(timed_launch(RA_KERNEL_ATTN_BWD, stream, [&] { return launch_bwd_bf16(st, D, stream); }));
     if (t >= 1) {
@@ -526,7 +531,6 @@ static int run_bwd_host(const void* q_blk, const void* k_all, const void* v_all,
   if ((rc = R.event(&tail))) return rc;
   RA_HIP(hipEventRecord(tail, side));
   RA_HIP(hipStreamWaitEvent(stream, tail, 0));
-  RA_HIP(launch_cast_f32_bf16(dq32, dq_blk, (long long)qel, stream));
   return RA_OK;
 }
 
