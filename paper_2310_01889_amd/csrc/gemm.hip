@@ -2,9 +2,11 @@
 //
 // C[M][N] = sum_k A[m][k] B[k][n] with A stored row-major [M][K] (TA = 0) or as its
 // transpose [K][M] (TA = 1), B stored row-major [K][N] (TB = 0) or as [N][K] (TB = 1).
-// Workgroup tile 256 x 256, 4 waves each owning a 128 x 128 sub-tile (16 accumulators of
-// 32 x 32).  K advances 32 at a time through a ring of five LDS stages (all 160 KB of
-// the CU's LDS) filled by direct-to-LDS buffer loads four steps ahead of their use.  Tiles are kept in their
+// Workgroup tile 256 x 256, 8 waves (two per SIMD) each owning a 128 x 64 sub-tile (8
+// accumulators of 32 x 32): while one wave waits for operands or the barrier, the other
+// keeps the matrix core busy.  K advances 32 at a time through a ring of five LDS stages
+// (all 160 KB of the CU's LDS) filled by direct-to-LDS buffer loads four steps ahead of
+// their use.  Tiles are kept in their
 // memory layout, unpadded, with 16-byte chunks XOR-swizzled per row so that both the row
 // reads and the transpose reads (an operand whose registers must run along its contiguous
 // dimension) are free of bank conflicts.  Each wave computes C^T = B^T A^T so that a lane
@@ -18,7 +20,7 @@
 namespace ra {
 namespace {
 
-constexpr int kTM = 256, kTN = 256, kTK = 32, kGT = 256;
+constexpr int kTM = 256, kTN = 256, kTK = 32, kGT = 512;
 constexpr int kNS = 5;                      // ring stages
 constexpr int kTileB = 256 * kTK * 2;       // bytes of one operand tile (16 KB)
 constexpr int kLoadsPerTile = kTileB / 1024 / (kGT / 64);  // 1 KB loads per wave per tile
@@ -93,14 +95,14 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
   const int m0 = tm * kTM, n0 = tn * kTN;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;  // 128 rows x 64 columns per wave
   const bf16* A = (const bf16*)g.A;
   const bf16* B = (const bf16*)g.B;
   const int nk = g.K / kTK;
 
-  f32x16 acc[4][4];  // [n tile][m tile] of C^T
+  f32x16 acc[2][4];  // [n tile][m tile] of C^T
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
@@ -147,14 +149,20 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) roff[kk] = l32 * 64 + 16 * ((2 * kk + hi) ^ swz_row(l32));
   // k-major operand by transpose reads: rows 16 kk + 8 hi + li / 4 (and + 4), columns
-  // base + 32 t + 16 (gq & 1) + 4 (li & 3) for t = 0..3 (base a multiple of 128)
+  // base + 32 t + 16 (gq & 1) + 4 (li & 3) for t = 0..3 (A: base 128 wm, a multiple of 128,
+  // which the swizzle leaves in place) or t = 0..1 (B: columns 64 wn + ..., swizzled whole)
   const int gq = lane >> 4, li = lane & 15;
   const int trow = 8 * hi + (li >> 2);
-  int toff[4];
+  int toff[4], tboff[2];
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int col = 32 * t + 16 * (gq & 1) + 4 * (li & 3);
     toff[t] = trow * 512 + 16 * ((col >> 3) ^ swz_kmaj(trow)) + 2 * (col & 7);
+  }
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int col = 64 * wn + 32 * t + 16 * (gq & 1) + 4 * (li & 3);
+    tboff[t] = trow * 512 + 16 * ((col >> 3) ^ swz_kmaj(trow)) + 2 * (col & 7);
   }
   // operand fetch for k-slice kk of a stage: A operand rows m (bop: B^T rows n)
   auto fetch = [&](const char* st, int kk, bf16x8* aop, bf16x8* bop) __attribute__((always_inline)) {
@@ -169,10 +177,13 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
         const bf16x4 lo = lds_read_tr16((const bf16*)p), up = lds_read_tr16((const bf16*)(p + 4 * 512));
         aop[i] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
       }
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
       if (TB) {
-        bop[i] = *(const bf16x8*)(bs + (wn * 128 + 32 * i) * 64 + roff[kk]);
+        bop[i] = *(const bf16x8*)(bs + (wn * 64 + 32 * i) * 64 + roff[kk]);
       } else {
-        const char* p = bs + kk * 16 * 512 + wn * 256 + toff[i];
+        const char* p = bs + kk * 16 * 512 + tboff[i];
         const bf16x4 lo = lds_read_tr16((const bf16*)p), up = lds_read_tr16((const bf16*)(p + 4 * 512));
         bop[i] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
       }
@@ -191,7 +202,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
   // (those of kt+2 .. kt+4 may stay in flight -- loads complete in issue order), the
   // barrier (every read of this stage has been issued by now), and step kt+1's slice-0
   // reads, covered by slice 1's products.
-  bf16x8 a0[4], b0[4], a1[4], b1[4];
+  bf16x8 a0[4], b0[2], a1[4], b1[2];
 #pragma unroll
   for (int s = 0; s < kNS - 1; ++s)
     if (s < nk) {
@@ -207,7 +218,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
     constexpr int S = decltype(Sc)::value;
     if (kt + kNS - 1 < nk) load_stage(kt + kNS - 1, std::integral_constant<int, (S + kNS - 1) % kNS>{});
     fetch(stage(Sc), 1, a1, b1);
-    mfmas(a0, b0, 0, 4);
+    mfmas(a0, b0, 0, 2);
     // step kt+1 must have landed: at most the loads of steps kt+2 .. kt+4 outstanding
     constexpr int LPS = 2 * kLoadsPerTile;  // loads per step per wave
     if (kt + 4 < nk)
@@ -220,7 +231,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_barrier();
     if (kt + 1 < nk) fetch(stage(std::integral_constant<int, S + 1>{}), 0, a0, b0);
-    mfmas(a1, b1, 0, 4);
+    mfmas(a1, b1, 0, 2);
   };
   int kt = 0;
   for (; kt + kNS - 1 < nk; kt += kNS) {
@@ -240,7 +251,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
   // passes of 128 rows: the two waves owning those rows write them, 32 rows per stage
   // buffer (1 KB rows; 16-byte chunk c of row r stored at c ^ (r & 15), so both the
   // writes -- 32 rows at one column -- and the row reads are free of bank conflicts);
-  // then every wave takes 8 rows of each buffer and a lane handles 4 consecutive columns,
+  // then every wave takes 4 rows of each buffer and a lane handles 4 consecutive columns,
   // so bias, residual, pre-activation and output accesses are contiguous along rows.
   auto epi4 = [&](int m, int n, float* v) __attribute__((always_inline)) {
     const long long off = (long long)m * g.ldc + n;
@@ -298,15 +309,15 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
   for (int pass = 0; pass < 2; ++pass) {
     if (wm == pass) {
       // lane: row 32 mi + l32 of the pass (stage buffer mi, local row l32), columns
-      // 128 wn + 32 ni + 8 q4 + 4 hi .. +3 (chunk 32 wn + 8 ni + 2 q4 + hi)
+      // 64 wn + 32 ni + 8 q4 + 4 hi .. +3 (chunk 16 wn + 8 ni + 2 q4 + hi)
       static_for<0, 4>([&](auto Mi) __attribute__((always_inline)) {
         constexpr int mi = decltype(Mi)::value;
         char* sb = stage(std::integral_constant<int, mi>{}) + l32 * 1024;
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
+        for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
           for (int q4 = 0; q4 < 4; ++q4) {
-            const int c = 32 * wn + 8 * ni + 2 * q4 + hi;
+            const int c = 16 * wn + 8 * ni + 2 * q4 + hi;
             *(f32x4*)(sb + 16 * (c ^ (l32 & 15))) =
                 f32x4{acc[ni][mi][4 * q4], acc[ni][mi][4 * q4 + 1], acc[ni][mi][4 * q4 + 2], acc[ni][mi][4 * q4 + 3]};
           }
@@ -317,8 +328,8 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(const GemmArgs g) {
       constexpr int bi = decltype(Bi)::value;
       const char* sb = stage(std::integral_constant<int, bi>{});
 #pragma unroll 2
-      for (int rr = 0; rr < 8; ++rr) {
-        const int lr = 8 * wave + rr;  // local row of the buffer
+      for (int rr = 0; rr < 4; ++rr) {
+        const int lr = 4 * wave + rr;  // local row of the buffer
         const f32x4 t = *(const f32x4*)(sb + lr * 1024 + 16 * (lane ^ (lr & 15)));
         float v[4] = {t[0], t[1], t[2], t[3]};
         epi4(m0 + 128 * pass + 32 * bi + lr, n0 + 4 * lane, v);
