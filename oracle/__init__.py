@@ -30,11 +30,15 @@ Modules
   layer      -- one transformer layer as Algorithm 1 composes it: projections,
                 ring attention, output projection with residual, blockwise FFN with
                 residual; forward and backward.
+  overlap    -- Section 3's arithmetic intensity between hosts: the block size at which
+                a ring step's attention work hides the key/value transfer (c >= F/B) and
+                the minimal sequence per host (6c).
 
 Every function takes and returns float64 arrays.  Inputs in bf16 are passed in already
 rounded (the exact values the GPU sees), then upcast.
 
-Parity status: attention forward/backward, ring bookkeeping, ring decode and FFN are pinned by the
+Parity status: attention forward/backward, ring bookkeeping, ring decode, FFN and the overlap
+condition (against the paper's printed table, tests/golden/) are pinned by the
 tests in tests/test_oracle_*.py (closed forms, invariants, brute force, finite
 differences, library routines).  The layer composition is pinned only to the
 composition defined in ``layer`` (the paper does not fix norms, biases or the
