@@ -13,9 +13,11 @@
  *
  * On one GPU the ring is virtual: all hosts' blocks live in device memory; each call
  * runs n_hosts ring steps, each one kernel launch covering every host that has work at
- * that step, and before each step the blocks that every host will need next are copied
- * into a per-host receive buffer (double buffer) on a library-owned side stream,
- * overlapping the compute of the current step.
+ * that step, and the block each host needs at the next step reaches its per-host receive
+ * buffer (double buffer) during the current step: in bf16 calls over the whole ring the
+ * step kernels write it there themselves (each host sends the block it holds to the next
+ * host); otherwise (one host's share, float32) device-to-device copies on a
+ * library-owned side stream bring it in, overlapping the compute of the current step.
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless stated.  The caller allocates and owns every
@@ -32,7 +34,7 @@
  *     global position p sees key at global position p' iff p' <= p; masked keys
  *     contribute exactly zero and fully masked blocks are skipped.
  *   - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t; NULL means
- *     the legacy default stream).  Work on the side stream is joined back to `stream`
+ *     the legacy default stream).  Work on a side stream is joined back to `stream`
  *     by events, so callers see single-stream semantics.  Distinct streams may be used
  *     from distinct threads concurrently.
  *   - Workspace (receive buffers, float32 accumulators) is allocated stream-ordered on
