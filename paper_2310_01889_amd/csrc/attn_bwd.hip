@@ -18,11 +18,12 @@ namespace {
 
 // -------------------------------------------------------------------------------------
 // Delta_r = sum_d dO_rd * O_rd  (float32 [B, H, S]); rows in memory order (b, r, h).
-// The bf16 step kernels take -Delta and -lse log2e (their accumulators start there).
+// The bf16 step kernels take -Delta and -lse sqrt(D) (their accumulators start there:
+// the score accumulators hold q.k, in units of the unscaled products).
 // -------------------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const bf16* dO, const float* lse,
-                                                           float* ndelta, float* nlse2, int B, int S, int H) {
+                                                           float* ndelta, float* nlse_s, int B, int S, int H) {
   constexpr int TPR = D / 8;  // threads per row
   const long long row = (long long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
   const int c = (threadIdx.x % TPR) * 8;
@@ -41,7 +42,7 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const 
     const int r = (int)(br % S), b = (int)(br / S);
     const long long idx = ((long long)b * H + h) * S + r;
     ndelta[idx] = -s;
-    nlse2[idx] = -lse[idx] * kLog2e;  // the bf16 step kernels work in log2 units
+    nlse_s[idx] = -lse[idx] * sqrtf((float)D);  // lse / scale: units of q.k
   }
 }
 
@@ -71,10 +72,10 @@ __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const 
 // =====================================================================================
 // bf16 dK/dV kernel: 4 waves x 32 keys = 128 keys per workgroup; loops over 32-query
 // tiles of the host's block.  Per wave, lanes run over the wave's keys:
-//   S' = Q (K log2e/sqrt(D))^T - lse log2e   [query x key] (A = Q rows from LDS with
-//        row bits 2 and 3 swapped, B = the pre-scaled K of the wave's keys in registers;
-//        the accumulator starts at -lse log2e of its query, so S' comes out ready)
-//   P  = exp2(S')                                               (masked -> 0)
+//   S' = Q K^T - lse sqrt(D)   [query x key] (A = Q rows from LDS with row bits 2 and 3
+//        swapped, B = K of the wave's keys in registers, as stored: the products are
+//        exact in float32; the accumulator starts at -lse sqrt(D) of its query)
+//   P  = exp2(S' log2e / sqrt(D))  (the scale in float32)       (masked -> 0)
 //   dP = dO V^T - Delta   (A = dO rows, B = V in registers; starts at -Delta)
 //   dS = P * dP
 //   dV^T += dO^T P        (A = dO^T by LDS transpose read, B = P)
@@ -102,7 +103,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
   __shared__ __attribute__((aligned(1024))) bf16 sO2[kQB * D];
   // lse * log2e and Delta: 64 floats each, as a one-wave 4-byte load writes 256 bytes
   // (lanes past the tile read zero)
-  __shared__ __attribute__((aligned(256))) float sL0[64];  // -lse log2e
+  __shared__ __attribute__((aligned(256))) float sL0[64];  // -lse sqrt(D)
   __shared__ __attribute__((aligned(256))) float sL1[64];
   __shared__ __attribute__((aligned(256))) float sL2[64];
   __shared__ __attribute__((aligned(256))) float sD0[64];  // -Delta
@@ -149,8 +150,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       *(bf16x8*)(fkrow + 16 * kk + 8 * hi) = kx;
       *(bf16x8*)(fvrow + 16 * kk + 8 * hi) = vreg[kk];
     }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) kreg[kk][e] = (bf16)((float)kx[e] * sl2);  // scores in log2 units
+    kreg[kk] = kx;
   }
   f32x16 dkacc[NDT], dvacc[NDT];
 #pragma unroll
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
       toff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
 
-  // accumulator starts of S' (-lse log2e) and dP (-Delta), stored negated by the
+  // accumulator starts of S' (-lse sqrt(D)) and dP (-Delta), stored negated by the
   // preprocess kernel, of a tile: register 8 g + e of a lane holds query 16 g + 8 hi + e
   auto inits = [&](auto Bc, f32x16& si, f32x16& di) __attribute__((always_inline)) {
     const float* sl = pick(Bc, sL0, sL1, sL2);
@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int r = 8 * g + 2 * u + e;
-      float pr = fast_exp2(sc[r]);
+      float pr = fast_exp2(sc[r] * sl2);
       if (MASK && kpos > qpos0 + 16 * g + 8 * hi + 2 * u + e) pr = 0.f;
       pv[e] = pr;
       dsv[e] = pr * dpc[r];
@@ -424,7 +424,8 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
 //   S^T  = K Q^T            (A = K rows from LDS, B = Q in registers)
 //   dP^T = V dO^T - Delta   (A = V rows, B = dO in registers; the accumulator starts at
 //                            -Delta of the lane's query, so the subtraction is free)
-//   P^T  = exp2(S^T log2e/sqrt(D) - lse log2e),  dS^T = P^T * dP^T   (masked -> 0)
+//   P^T  = exp2(S^T log2e/sqrt(D) - lse log2e),  dS^T = P^T * dP^T   (masked -> 0), the
+//          scale applied in float32
 //   dQ^T += K^T dS^T        (A = K^T by LDS transpose read, B = dS^T)
 // K and V tiles are filled by direct-to-LDS buffer loads into XOR-swizzled unpadded rows
 // (see swz), double buffered: tile it+1 streams in while tile it is processed.
@@ -461,7 +462,7 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   const int qpos = hs.q_pos0 + qt * kQQ + wave * 32 + l32;
   const int tile_first_q = hs.q_pos0 + qt * kQQ;
   const long long lrow = (long long)bh * p.Sq + qr;
-  const float nlse2 = p.lse[lrow];  // -lse * log2e (written by the preprocess kernel)
+  const float nlse_s = p.lse[lrow];  // -lse sqrt(D) (written by the preprocess kernel)
   const float ndlt = p.delta[lrow];  // -Delta
 
   bf16x8 qreg[NKK], oreg[NKK];
@@ -524,6 +525,7 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
       toff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
   const float sl2 = p.scale * kLog2e;
+  const float nl2 = nlse_s * sl2;  // -lse log2(e): the exponent is q.k sl2 + nl2 in float32
 
   auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
     constexpr int B = decltype(Bc)::value;
@@ -556,7 +558,7 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
         for (int e = 0; e < 2; ++e) {
           const int i = 8 * (kb & 1) + 2 * j + e;
           const int mt = kb >> 1;
-          float pv = fast_exp2(fmaf(sacc[mt][i], sl2, nlse2));
+          float pv = fast_exp2(fmaf(sacc[mt][i], sl2, nl2));
           if (MASK) {
             const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
             if (kpos > qpos) pv = 0.f;
@@ -767,15 +769,15 @@ __global__ void zero_f32_kernel(float* p, long long n) {
 
 }  // namespace
 
-hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, float* delta, float* lse2, int B,
+hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, float* delta, float* nlse_s, int B,
                                int S, int H, int D, hipStream_t st) {
   const long long rows = (long long)B * S * H;
   const int rpb = 256 / (D / 8);
   const long long blocks = (rows + rpb - 1) / rpb;
   if (D == 128)
-    hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, lse2, B, S, H);
+    hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, nlse_s, B, S, H);
   else
-    hipLaunchKernelGGL(bwd_pre_bf16_kernel<64>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, lse2, B, S, H);
+    hipLaunchKernelGGL(bwd_pre_bf16_kernel<64>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, nlse_s, B, S, H);
   return hipGetLastError();
 }
 

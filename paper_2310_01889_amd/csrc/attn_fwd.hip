@@ -127,28 +127,28 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   }
 
   // ---- Q in registers: B operand of S^T = K Q^T (n = query, k = dim) ---------------
-  // Q is stored pre-multiplied by log2(e)/sqrt(D) (rounded to bf16), so the products
-  // come out as scaled scores in log2 units.
+  // Q as stored (bf16): the products q.k are exact in the float32 accumulators, and the
+  // scale log2(e)/sqrt(D) is applied in float32 (the paper's float32 logits), once per
+  // score, right before its exponential.
   const float sl2 = p.scale * kLog2e;
+  const float isl2 = 1.f / sl2;
   bf16x8 qreg[NKK];
   {
     const bf16* qrow = qbase + (long long)qr * rs;
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) {
-      const bf16x8 t = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qreg[kk][e] = (bf16)((float)t[e] * sl2);
-    }
+    for (int kk = 0; kk < NKK; ++kk) qreg[kk] = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
   }
-  // The score accumulators start from -m_eff (m_eff = running maximum, 0 while it is
-  // still -inf), so each MFMA chain yields s - m_eff directly.  thr: a row whose new
-  // scores exceed it forces a rescale (kTau above the maximum, any visible key at all
-  // while the maximum is still -inf).
+  // Scores in log2 units are sl2 * q.k.  The score accumulators start from -m_eff / sl2
+  // (m_eff = running maximum in log2 units, 0 while it is still -inf), so each MFMA chain
+  // yields (s - m_eff) / sl2, and one multiply as soon as a tile's chains are complete
+  // gives s - m_eff, the exponent.  thr: a row whose new scores exceed it forces a
+  // rescale (kTau above the maximum, any visible key at all while the maximum is still
+  // -inf).
   float m_eff = (m_run == -INFINITY) ? 0.f : m_run;
   float thr = (m_run == -INFINITY) ? -INFINITY : kTau;
   f32x16 minit;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) minit[i] = -m_eff;
+  for (int i = 0; i < 16; ++i) minit[i] = -m_eff * isl2;
 
   // ---- direct-to-LDS staging: each wave fills 16 rows of a tile ---------------------
   // load j of a wave covers rows wave*RPW + j*ROWS_PER_LOAD + lane / CPR; the lane's
@@ -209,8 +209,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   // lane l^32 holds the other half of its keys.  The running maximum is raised only
   // when a row's new scores exceed it by more than kTau, so probabilities stay below
   // 2^kTau and the rescale of the accumulator -- a wave-uniform branch -- is rare.
-  // mx: this lane's maximum of the tile's s - m_eff; sc: the tile's scores, shifted here
-  // to the new maximum.
+  // mx: this lane's maximum of the tile's s - m_eff; sc: the tile's scores (s - m_eff,
+  // log2 units), shifted here to the new maximum.
   auto rescale = [&](float mx, f32x16* sc) __attribute__((always_inline)) {
     const float mx2 = pair_max(mx);
     if (__builtin_amdgcn_ballot_w64(mx2 > thr)) {
@@ -231,8 +231,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       m_eff = m_new_eff;
       thr = (m_new == -INFINITY) ? -INFINITY : kTau;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) minit[i] = -m_eff;
+      for (int i = 0; i < 16; ++i) minit[i] = -m_eff * isl2;
     }
+  };
+  auto scale_half = [&](f32x16* sc, int mt) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sc[mt][i] *= sl2;
   };
   auto decide = [&](f32x16* sc) __attribute__((always_inline)) {
     float mx = -INFINITY;
@@ -295,6 +299,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   f32x16 s_cur[2];
   if (nt > 0) {
     scores(sK0, s_cur);
+    scale_half(s_cur, 0);
+    scale_half(s_cur, 1);
     if (n_full == 0) mask(s_cur, 0);
     decide(s_cur);
   }
@@ -366,10 +372,12 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
         rs2[P % 4] = dot2_bf16_ones(w[P / 4][P % 4], rs2[P % 4]);  // row sum of the bf16 probabilities used
       }
       if constexpr (S == 16 || S == 17) {
+        if constexpr (S == 16) scale_half(s_next, 0);
         if constexpr (S == 16 && MN) mask_half(s_next, 0, it + 1);
 #pragma unroll
         for (int i = 8 * (S - 16); i < 8 * (S - 15); ++i) mxa = fmaxf(mxa, s_next[0][i]);
       } else if constexpr (S >= 18) {
+        if constexpr (S == 18) scale_half(s_next, 1);
         if constexpr (S == 18 && MN) mask_half(s_next, 1, it + 1);
         if constexpr (S < 20) {
 #pragma unroll
@@ -393,6 +401,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     load_v(it + 1, std::integral_constant<int, B ^ 1>{});
     f32x16 s_next[2];
     scores(kbuf(std::integral_constant<int, B ^ 1>{}), s_next);
+    scale_half(s_next, 0);
+    scale_half(s_next, 1);
     softmax_pv(s_cur, vbuf(Bc));
     if (MN) mask(s_next, it + 1);
     decide(s_next);

@@ -38,8 +38,8 @@ struct DecodeArgs {
 // One wave: the partial state of all Tq queries (lane l % 32 = query slot) over the kch
 // keys of one chunk.  The arithmetic per 32-key tile is that of the forward step kernel:
 // S^T = K Q^T on the matrix cores (K rows from LDS with bits 2 and 3 of the row index
-// swapped, Q pre-scaled by log2(e)/sqrt(D) in registers, accumulators starting at minus
-// the running maximum), lazy online softmax, O^T += V^T P^T with V^T read from LDS by
+// swapped, Q as stored in registers, accumulators starting at minus the running maximum
+// over the scale, which is applied in float32 before the maximum), lazy online softmax, O^T += V^T P^T with V^T read from LDS by
 // the transpose read.  Tiles are double buffered: direct-to-LDS loads of tile it+1 are
 // in flight while tile it is processed.  Lanes of slots >= Tq compute on zero queries
 // and store nothing.
@@ -67,7 +67,10 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(const DecodeArgs a) 
   const int k0 = ch * a.kch;
   const int nt = a.kch / kDecKT;
 
+  // scores in log2 units: sl2 q.k, the products exact in float32 (the queries stay as
+  // stored), the scale applied in float32
   const float sl2 = a.scale * kLog2e;
+  const float isl2 = 1.f / sl2;
   bf16x8 qreg[NKK];
   {
     const bf16* qrow = a.q + ((long long)b * a.Tq + min(t, a.Tq - 1)) * rs + h * D;
@@ -75,7 +78,7 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(const DecodeArgs a) 
     for (int kk = 0; kk < NKK; ++kk) {
       const bf16x8 x = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qreg[kk][e] = (bf16)(t < a.Tq ? (float)x[e] * sl2 : 0.f);
+      for (int e = 0; e < 8; ++e) qreg[kk][e] = t < a.Tq ? x[e] : (bf16)0.f;
     }
   }
 
@@ -137,6 +140,8 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(const DecodeArgs a) 
     f32x16 s = mfma32(*(const bf16x8*)(kt + koff[0]), qreg[0], minit);
 #pragma unroll
     for (int kk = 1; kk < NKK; ++kk) s = mfma32(*(const bf16x8*)(kt + koff[kk]), qreg[kk], s);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s[i] *= sl2;  // s - m_eff, log2 units
     const int kpos0 = k0 + it * kDecKT;
     if (a.causal && kpos0 + kDecKT - 1 > a.S - a.Tq) {
 #pragma unroll
@@ -164,7 +169,7 @@ __global__ __launch_bounds__(64) void decode_partial_kernel(const DecodeArgs a) 
       m_eff = m_new_eff;
       thr = (m_new == -INFINITY) ? -INFINITY : kDecTau;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) minit[i] = -m_eff;
+      for (int i = 0; i < 16; ++i) minit[i] = -m_eff * isl2;
     }
     // P (bf16) and O^T += V^T P^T, one 16-key group at a time
 #pragma unroll

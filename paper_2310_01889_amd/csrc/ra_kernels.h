@@ -57,7 +57,7 @@ struct BwdStep {
   StepHost host[kMaxSlots];
   const void* q;          // [B, Sq, H, D]
   const void* dO;         // [B, Sq, H, D]
-  const float* lse;       // [B, H, Sq]  lse, natural log (float32 kernels); -lse log2(e) (bf16)
+  const float* lse;       // [B, H, Sq]  lse, natural log (float32 kernels); -lse sqrt(D) (bf16)
   const float* delta;     // [B, H, Sq]  rowsum(dO * o) (float32 kernels); its negative (bf16)
   float* dq;              // float32 [B, Sq, H, D]
   float* dk;              // float32 [B, Skv, H, D]: gradient of the block each host holds
@@ -82,8 +82,8 @@ struct BwdStep {
 
 hipError_t launch_fwd_bf16(const FwdStep& s, int D, hipStream_t st);
 hipError_t launch_fwd_f32(const FwdStep& s, int D, hipStream_t st);
-// -Delta = -rowsum(dO * o) and -lse * log2(e), both [B, H, S] (for the bf16 step kernels)
-hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, float* ndelta, float* nlse2,
+// -Delta = -rowsum(dO * o) and -lse * sqrt(D), both [B, H, S] (for the bf16 step kernels)
+hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, float* ndelta, float* nlse_s,
                                int B, int S, int H, int D, hipStream_t st);
 hipError_t launch_bwd_pre_f32(const float* o, const float* dO, float* delta, int B, int S, int H,
                               int D, hipStream_t st);

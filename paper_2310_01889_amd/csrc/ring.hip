@@ -334,7 +334,7 @@ static int run_bwd(const RingProblem& P, const void* o, const float* lse, const 
   if (rc) return rc;
   char* base = (char*)R.ws;
   float* delta = (float*)(base + recv);
-  float* lse2 = delta + nrow;  // bf16 path: lse in log2 units
+  float* lse2 = delta + nrow;  // bf16 path: -lse sqrt(D), in units of q.k
   float* gq = f32 ? (float*)dq : lse2 + nrow;
   float* gk = f32 ? (float*)dk : gq + telems;
   float* gv = f32 ? (float*)dv : gk + telems;

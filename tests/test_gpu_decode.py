@@ -23,9 +23,10 @@ pytestmark = pytest.mark.gpu
 TOL = 2e-2
 
 
-def _case(seed, B, S, H, D, Tq, N, causal):
-    log("decode case seed=%d B=%d S=%d H=%d D=%d Tq=%d N=%d causal=%d" % (seed, B, S, H, D, Tq, N, causal))
+def _case(seed, B, S, H, D, Tq, N, causal, amp=1.0):
+    log("decode case seed=%d B=%d S=%d H=%d D=%d Tq=%d N=%d causal=%d amp=%g" % (seed, B, S, H, D, Tq, N, causal, amp))
     q, k, v = synth.attention_inputs(seed, B, Tq, H, D, kv_len=S)
+    q = q * amp  # a power of two: exact in bf16
     o, lse = ra.attention_decode(*dev(q, k, v), N, causal)
     torch.cuda.synchronize()
     o_ref, lse_ref = OD.ring_decode_fwd(np64(q), np64(k), np64(v), N, bool(causal))
@@ -89,3 +90,11 @@ def test_decode_full_size_sampled_heads(Tq):
         eo, el = max_err(o[:, :, sl], o_ref), max_err(lse[:, sl], lse_ref)
         log("   head %d: max|o err| %.3e  max|lse err| %.3e" % (h, eo, el))
         assert eo <= TOL and el <= TOL
+
+
+@pytest.mark.parametrize("amp", [4.0, 8.0])
+def test_decode_large_logits(amp):
+    """Scores of standard deviation 4 and 8: the products are exact in float32 and the scale
+    is applied in float32, so the error does not grow with the logit scale."""
+    eo, el, _ = _case(90, 1, 4096, 2, 128, 8, 4, 1, amp)
+    assert eo <= TOL and el <= TOL
