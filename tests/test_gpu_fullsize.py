@@ -121,3 +121,47 @@ def test_causal_forward_backward_S16384_H16_hosts8():
         eg = [max_err(t[:, :, h:h + 1], r) for t, r in zip((dq, dk, dv), g_ref)]
         log("   head %d: o %.3e lse %.3e dq/dk/dv %s" % (h, eo, el, ["%.3e" % x for x in eg]))
         assert eo <= TOL_O and el <= TOL_O and max(eg) <= TOL_G
+
+
+def test_blockwise_ffn_full_size_sampled():
+    """Blockwise FFN at the benchmarked size (T = 65536 in 8 blocks of 8192, d_model 4096,
+    d_ff 16384, GeLU, no bias), forward and backward.  The FFN acts row by row, so rows of
+    y and dx come from the oracle on those rows alone; a column j of dW1 (and row j of dW2,
+    entry j of db1) depends only on column j of W1 and row j of W2, so the oracle on a
+    narrow FFN made of sampled hidden units gives them exactly.  Tolerances as in
+    test_gpu_ffn.py: |err| <= 2e-2 (y) / 5e-2 (dx) times max(1, |ref|); weight gradients
+    max |err| <= 5e-2 * max(1, rms(ref))."""
+    from oracle import ffn as OF
+    T, dm, dff, blk, act = 65536, 4096, 16384, 8192, ra.ACT_GELU_ERF
+    x, w1, _, w2, _, dy = synth.ffn_inputs(61, T, dm, dff, with_grad=True)
+    xd, w1d, w2d, dyd = dev(x, w1, w2, dy)
+    y = torch.empty((T, dm), dtype=torch.bfloat16, device="cuda")
+    ra.blockwise_ffn(xd, w1d, None, w2d, None, y, blk, act)
+    dx = torch.empty_like(xd)
+    dw1 = torch.empty((dm, dff), dtype=torch.float32, device="cuda")
+    db1 = torch.empty((dff,), dtype=torch.float32, device="cuda")
+    dw2 = torch.empty((dff, dm), dtype=torch.float32, device="cuda")
+    db2 = torch.empty((dm,), dtype=torch.float32, device="cuda")
+    ra.blockwise_ffn_bwd(xd, w1d, None, w2d, dyd, dx, dw1, db1, dw2, db2, blk, act)
+    torch.cuda.synchronize()
+
+    rows = _sample_rows(12, T, [0, blk - 1, blk, T - 1])
+    log("ffn full size: rows %s" % rows.tolist())
+    y_ref = OF.ffn_fwd(np64(x[rows]), np64(w1), None, np64(w2), None, act)
+    dx_ref = OF.ffn_bwd(np64(x[rows]), np64(w1), None, np64(w2), np64(dy[rows]), act)[0]
+    ey = np.abs(np64(y[rows].cpu()) - y_ref) / np.maximum(1.0, np.abs(y_ref))
+    ex = np.abs(np64(dx[rows].cpu()) - dx_ref) / np.maximum(1.0, np.abs(dx_ref))
+    log("  y scaled err %.3e  dx scaled err %.3e" % (ey.max(), ex.max()))
+    assert ey.max() <= 2e-2 and ex.max() <= 5e-2
+
+    cols = np.array(sorted(set([0, dff - 1]) | set(np.random.default_rng(5).integers(0, dff, 4).tolist())))
+    _, rdw1, rdb1, rdw2, rdb2 = OF.ffn_bwd(np64(x), np64(w1[:, cols]), None, np64(w2[cols, :]), np64(dy), act)
+    for name, got, ref in (("dW1 cols", dw1[:, cols], rdw1), ("db1", db1[cols], rdb1), ("dW2 rows", dw2[cols, :], rdw2)):
+        g, r = np64(got.cpu()), np.asarray(ref)
+        bound = 5e-2 * max(1.0, float(np.sqrt(np.mean(r * r))))
+        log("  %s: max|err| %.3e bound %.3e" % (name, np.abs(g - r).max(), bound))
+        assert np.abs(g - r).max() <= bound
+    # db2 = column sums of dy (no hidden unit involved)
+    e2 = np.abs(np64(db2.cpu()) - rdb2).max()
+    log("  db2: max|err| %.3e" % e2)
+    assert e2 <= 5e-2 * max(1.0, float(np.sqrt(np.mean(rdb2 * rdb2))))
