@@ -196,3 +196,25 @@ def test_llama_layer_model_width_short_sequence():
         rr = _rel_rms(g, r)
         log("   %s rel rms %.3e" % (n, rr))
         assert rr <= 2e-2 and _grad_ok(g, r, 8e-2, name=n)
+
+
+@pytest.mark.slow
+def test_llama_layer_full_size_forward_sampled_rows():
+    """The benchmarked size (S = 65536 in 8 host blocks of 8192, d_model 4096 = 32 heads x 128,
+    d_ff 11008): rows of z in the first host block and at the start of the second, against
+    the oracle layer on the prefix x[:8200] -- a causal row depends only on the rows before
+    it, and the prefix keeps the positions (RoPE) of the full sequence.  Bounds as the
+    model-width test: relative RMS <= 2e-2, max scaled <= 1.2e-1."""
+    S, dm, H, dff, N = 65536, 4096, 32, 11008, 8
+    x, layers, _, xd, pd, _ = _run_layer(440, S, dm, H, dff, N)
+    z = torch.empty_like(xd)
+    ra.llama_layer_fwd(xd, pd[0], z, H, N)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 777, 4095, 8191, 8192, 8199])
+    rmax = int(rows.max()) + 1
+    p64 = [np64(t) for t in layers[0]]
+    z_ref = OL.layer_fwd(np64(x[:rmax]), *p64, H)[rows]
+    zs = z[torch.from_numpy(rows).cuda()]
+    ez, rz = _scaled_err(zs, z_ref), _rel_rms(zs, z_ref)
+    log("   sampled z scaled err %.3e rel rms %.3e" % (ez, rz))
+    assert rz <= 2e-2 and ez <= 1.2e-1
