@@ -22,6 +22,8 @@ int set_err(int code, const char* fmt, ...);
                      #expr, hipGetErrorString(e_));                                    \
   } while (0)
 
+void keep_pool();
+
 // Stream-ordered workspace and events owned by one call; released on every exit path.
 struct CallResources {
   hipStream_t stream;
@@ -34,6 +36,7 @@ struct CallResources {
   }
   int alloc(size_t bytes) {
     if (bytes == 0) return RA_OK;
+    keep_pool();
     RA_HIP(hipMallocAsync(&ws, bytes, stream));
     return RA_OK;
   }

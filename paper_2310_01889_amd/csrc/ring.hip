@@ -52,17 +52,29 @@ int side_stream(hipStream_t* out) {
   RA_HIP(hipGetDevice(&dev));
   if (dev < 0 || dev >= 64) return set_err(RA_EHIP, "device index %d out of range", dev);
   std::lock_guard<std::mutex> lk(g_mu);
-  if (!g_side[dev]) {
-    RA_HIP(hipStreamCreateWithFlags(&g_side[dev], hipStreamNonBlocking));
-    // keep stream-ordered allocations cached in the pool between calls
-    hipMemPool_t pool;
-    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-      uint64_t thr = ~0ull;
-      (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
-    }
-  }
+  if (!g_side[dev]) RA_HIP(hipStreamCreateWithFlags(&g_side[dev], hipStreamNonBlocking));
   *out = g_side[dev];
   return RA_OK;
+}
+
+namespace {
+bool g_pool_kept[64];
+}  // namespace
+
+// Keep the current device's stream-ordered allocations cached in its default pool between
+// calls (release threshold: unlimited).  Otherwise the workspace freed at the end of a call
+// goes back to the driver at the next synchronisation and the next call maps it again.
+void keep_pool() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (g_pool_kept[dev]) return;
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+    uint64_t thr = ~0ull;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+  }
+  g_pool_kept[dev] = true;
 }
 
 // ---------------------------------------------------------------------------------
