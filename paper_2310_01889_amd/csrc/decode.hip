@@ -225,45 +225,70 @@ struct MergeArgs {
   int B, H, Tq, nch, n_hosts;
 };
 
-// One workgroup of 64 threads per (batch, head, query): combine the chunk partial
-// states in ring order -- blocks n_hosts-1, n_hosts-2, ..., 0, chunks of a block in
-// order.  All partials are present, so instead of carrying a running maximum the sum is
-// taken relative to the overall maximum M (found first, in any order):
+// One workgroup of 4 waves per (batch, head, query): combine the chunk partial states in
+// ring order -- blocks n_hosts-1, n_hosts-2, ..., 0, chunks of a block in order.  All
+// partials are present, so instead of carrying a running maximum the sum is taken relative
+// to the overall maximum M (found first, in any order):
 //   o = sum_c acc_c 2^(m_c - M) / sum_c l_c 2^(m_c - M),  lse = (M ln 2) + ln(denominator),
-// which is the online-softmax fold of the same partials in the same order, without its
-// sequential dependence; the loads of all chunks can then be in flight together.
+// which is the online-softmax fold of the same partials without its sequential
+// dependence.  Wave w sums the w-th quarter of the ring-ordered sequence of chunks, in
+// order; the four quarter sums are then added in order.  (A single wave walking every
+// chunk was bound by the latency of its dependent loads.)
+constexpr int kMergeWaves = 4;
+
 template <int D>
-__global__ __launch_bounds__(64) void decode_merge_kernel(const MergeArgs a) {
-  constexpr int E = D / 64;  // dims per thread
+__global__ __launch_bounds__(64 * kMergeWaves) void decode_merge_kernel(const MergeArgs a) {
+  constexpr int E = D / 64;  // dims per lane
+  __shared__ float s_max[kMergeWaves];
+  __shared__ float s_part[kMergeWaves][D + 1];
   const int t = blockIdx.x % a.Tq, bh = blockIdx.x / a.Tq;
   const int b = bh / a.H, h = bh % a.H;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int cpb = a.nch / a.n_hosts;  // chunks per block
   const long long base = (long long)bh * a.nch;
   float mx = -INFINITY;
-  for (int c = lane; c < a.nch; c += 64) mx = fmaxf(mx, a.part_m[(base + c) * a.Tq + t]);
+  for (int c = tid; c < a.nch; c += 64 * kMergeWaves) mx = fmaxf(mx, a.part_m[(base + c) * a.Tq + t]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  if (lane == 0) s_max[wave] = mx;
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kMergeWaves; ++w) mx = fmaxf(mx, s_max[w]);
+  // sequence position q (0 .. nch-1) of the ring order is chunk (n_hosts-1-q/cpb)*cpb + q%cpb
+  const int q0 = (int)((long long)a.nch * wave / kMergeWaves);
+  const int q1 = (int)((long long)a.nch * (wave + 1) / kMergeWaves);
   float l = 0.f, acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
-  for (int step = 0; step < a.n_hosts; ++step) {
-    const int blk = a.n_hosts - 1 - step;
 #pragma unroll 4
-    for (int c = 0; c < cpb; ++c) {
-      const long long row = (base + blk * cpb + c) * a.Tq + t;
-      const float mc = a.part_m[row];
-      const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - mx);
-      l = fmaf(a.part_l[row], w, l);
+  for (int q = q0; q < q1; ++q) {
+    const int chunk = (a.n_hosts - 1 - q / cpb) * cpb + q % cpb;
+    const long long row = (base + chunk) * a.Tq + t;
+    const float mc = a.part_m[row];
+    const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - mx);
+    l = fmaf(a.part_l[row], w, l);
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(a.part_acc[row * D + lane + 64 * e], w, acc[e]);
-    }
+    for (int e = 0; e < E; ++e) acc[e] = fmaf(a.part_acc[row * D + lane + 64 * e], w, acc[e]);
   }
-  const float inv = 1.f / l;
+#pragma unroll
+  for (int e = 0; e < E; ++e) s_part[wave][lane + 64 * e] = acc[e];
+  if (lane == 0) s_part[wave][D] = l;
+  __syncthreads();
+  if (wave != 0) return;
+  float lt = 0.f, at[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) at[e] = 0.f;
+#pragma unroll
+  for (int w = 0; w < kMergeWaves; ++w) {
+    lt += s_part[w][D];
+#pragma unroll
+    for (int e = 0; e < E; ++e) at[e] += s_part[w][lane + 64 * e];
+  }
+  const float inv = 1.f / lt;
   bf16* orow = a.o + ((long long)b * a.Tq + t) * a.H * D + h * D;
 #pragma unroll
-  for (int e = 0; e < E; ++e) orow[lane + 64 * e] = (bf16)(acc[e] * inv);
-  if (lane == 0) a.lse[(long long)bh * a.Tq + t] = mx * kLn2 + logf(l);
+  for (int e = 0; e < E; ++e) orow[lane + 64 * e] = (bf16)(at[e] * inv);
+  if (lane == 0) a.lse[(long long)bh * a.Tq + t] = mx * kLn2 + logf(lt);
 }
 
 // Keys per chunk: the whole block, halved while the launch has fewer than 4096
@@ -328,9 +353,9 @@ extern "C" int ring_attn_decode(const void* q, const void* k_cache, const void* 
   }));
   MergeArgs ma{da.part_acc, da.part_m, da.part_l, (bf16*)o, lse, B, H, Tq, nch, n_hosts};
   if (D == 128)
-    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(B * H * Tq), dim3(64), 0, stream, ma);
+    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(B * H * Tq), dim3(64 * kMergeWaves), 0, stream, ma);
   else
-    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(B * H * Tq), dim3(64), 0, stream, ma);
+    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(B * H * Tq), dim3(64 * kMergeWaves), 0, stream, ma);
   RA_HIP(hipGetLastError());
   return RA_OK;
 }
