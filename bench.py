@@ -3,8 +3,8 @@
 
 Workload (one "step"): causal ring-attention forward, B=1, S=32768, H=32, D=128, bf16
 inputs N(0,1), ring of 8 virtual hosts with 4096-token blocks -- partition and ring
-schedule, key/value rotation through the double buffer on the side stream, the
-attention-step kernel on every host, and finalisation.  Inputs are resident in HBM before
+schedule, the attention-step kernel on every host (whose workgroups also pass the
+key/value block each host holds into the next host's receive buffer), and finalisation.  Inputs are resident in HBM before
 the timed region.  Prints ONE JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra] [--only NAMES]
