@@ -7,10 +7,11 @@
 // host's block where it lies (a host's own block needs no transfer).  For t >= 1 the
 // block comes from that host's receive buffer: two slots used alternately (the
 // double buffer of the paper's memory accounting: current and receiving key/value
-// blocks).  The copies that fill the slot for step t+1 run on a library-owned side
-// stream while step t computes (the ppermute of the paper's code, overlapped with the
-// blockwise computation); events order every copy after the last reader of its slot
-// and every step after its copy.
+// blocks).  The slot for step t+1 is filled while step t computes (the ppermute of the
+// paper's code, overlapped with the blockwise computation): by the step-t kernels
+// themselves when a bf16 call covers the whole ring in ring order, otherwise by copies on
+// a library-owned side stream, with events ordering every copy after the last reader of
+// its slot and every step after its copy (see run_ring).
 #include <stdarg.h>
 #include <stdio.h>
 #include <stdlib.h>
