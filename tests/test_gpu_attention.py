@@ -247,15 +247,17 @@ def test_bf16_forward_large_logits(amp, D):
     assert eo <= TOL_O and el <= TOL_O
 
 
-def test_bf16_backward_large_logits():
+@pytest.mark.parametrize("D", [64, 128])
+def test_bf16_backward_large_logits(D):
     """Backward with scores of standard deviation 4 (queries scaled by 4): the recomputed
     probabilities use float32 scores.  The gradients grow with the scale (|dK| up to ~14
     here).  An fp64 emulation that rounds to bf16 exactly what this interface and path
     store in bf16 -- o as the entry point receives it (it enters Delta = rowsum(dO * o)),
     P and dS as product operands, the outputs -- leaves max errors of 2.3e-2 (dq), 7.8e-2
-    (dk; 7.0e-2 relative to max(1, |ref|)) and 3.5e-3 relative RMS: the bounds are 1e-1
-    on the magnitude-scaled error and 1e-2 relative RMS."""
-    B, S, H, D, N = 1, 1024, 2, 128, 4
+    (dk; 7.0e-2 relative to max(1, |ref|)) and 3.5e-3 relative RMS at D = 128 (D = 64: dk
+    5.6e-2 scaled, 3.3e-3 RMS): the bounds are 1e-1 on the magnitude-scaled error and 1e-2
+    relative RMS."""
+    B, S, H, N = 1, 1024, 2, 4
     q, k, v, do = synth.attention_inputs(13, B, S, H, D, with_grad=True)
     q = q * 4.0
     qd, kd, vd, dod = dev(q, k, v, do)
