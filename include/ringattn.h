@@ -46,7 +46,8 @@
  *
  * Supported shapes: D in {64, 128}; 1 <= n_hosts <= 64; S % n_hosts == 0; the block
  * c = S / n_hosts a multiple of 128 (bf16 attention) or 64 (float32 attention); B, H >= 1;
- * B * S * H * D < 2^31 elements per tensor.
+ * B * S * H * D < 2^31 elements per tensor.  ring_attn_fwd_varlen / ring_attn_bwd_varlen
+ * (causal, bf16) take any S >= 1; the limits then hold for the padded length.
  */
 #ifndef RINGATTN_H
 #define RINGATTN_H
@@ -90,6 +91,25 @@ int ring_attn_fwd(const void* q, const void* k, const void* v, void* o, float* l
 int ring_attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
                   const void* dO, void* dq, void* dk, void* dv,
                   int B, int H, int S, int D, int n_hosts, int causal, hipStream_t stream);
+
+/*
+ * Causal ring attention for any sequence length S >= 1 (Section 3: the sequence is cut into
+ * one block per host; here the last blocks may be short or empty), bf16.  The block is
+ * c = the smallest multiple of 128 with n_hosts * c >= S; the library stages q, k, v (and
+ * o, lse, dO) into zero-padded workspace copies of length n_hosts * c, runs the ring on
+ * them and copies the first S rows out.  Padded keys lie after every real query, so the
+ * causal mask hides them; padded query rows add exactly zero to dK and dV.  Arguments,
+ * layouts and outputs as ring_attn_fwd / ring_attn_bwd with causal = 1; S need not be a
+ * multiple of n_hosts or of 128 (when n_hosts * c == S no copies are made).  Workspace:
+ * 4 (forward) or 8 (backward) bf16 tensors [B, n_hosts * c, H, D] plus one float32
+ * [B, H, n_hosts * c], stream-ordered.  Errors: RA_EINVAL for null pointers or
+ * non-positive sizes, RA_EUNSUPPORTED when the padded shape is outside the supported set.
+ */
+int ring_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, float* lse,
+                         int B, int H, int S, int D, int n_hosts, hipStream_t stream);
+int ring_attn_bwd_varlen(const void* q, const void* k, const void* v, const void* o,
+                         const float* lse, const void* dO, void* dq, void* dk, void* dv,
+                         int B, int H, int S, int D, int n_hosts, hipStream_t stream);
 
 /* float32 twins of ring_attn_fwd / ring_attn_bwd: every tensor is float32, products and
  * accumulation are float32 (no bf16 rounding anywhere). */

@@ -39,6 +39,8 @@ _SIGS = {
     "ring_attn_fwd_f32": [_P] * 5 + [_I] * 6 + [_P],
     "ring_attn_bwd": [_P] * 9 + [_I] * 6 + [_P],
     "ring_attn_bwd_f32": [_P] * 9 + [_I] * 6 + [_P],
+    "ring_attn_fwd_varlen": [_P] * 5 + [_I] * 5 + [_P],
+    "ring_attn_bwd_varlen": [_P] * 9 + [_I] * 5 + [_P],
     "ring_attn_fwd_host": [_P] * 5 + [_I] * 7 + [_P],
     "ring_attn_bwd_host": [_P] * 9 + [_I] * 7 + [_P],
     "ring_attn_fwd_ordered": [_P] * 5 + [_I] * 6 + [_P, _P],
@@ -195,6 +197,21 @@ def ring_attn_bwd_f32(q, k, v, o, lse, dO, dq, dk, dv, n_hosts, causal, stream=N
     _call("ring_attn_bwd_f32", _ptr(q, f, "q"), _ptr(k, f, "k"), _ptr(v, f, "v"), _ptr(o, f, "o"),
           _ptr(lse, f, "lse"), _ptr(dO, f, "dO"), _ptr(dq, f, "dq"), _ptr(dk, f, "dk"), _ptr(dv, f, "dv"),
           B, H, S, D, int(n_hosts), int(causal), _stream(stream))
+
+
+def ring_attn_fwd_varlen(q, k, v, o, lse, n_hosts, stream=None):
+    B, S, H, D = _bshd(q)
+    bf = torch.bfloat16
+    _call("ring_attn_fwd_varlen", _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(o, bf, "o"),
+          _ptr(lse, torch.float32, "lse"), B, H, S, D, int(n_hosts), _stream(stream))
+
+
+def ring_attn_bwd_varlen(q, k, v, o, lse, dO, dq, dk, dv, n_hosts, stream=None):
+    B, S, H, D = _bshd(q)
+    bf = torch.bfloat16
+    _call("ring_attn_bwd_varlen", _ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"), _ptr(o, bf, "o"),
+          _ptr(lse, torch.float32, "lse"), _ptr(dO, bf, "dO"), _ptr(dq, bf, "dq"), _ptr(dk, bf, "dk"),
+          _ptr(dv, bf, "dv"), B, H, S, D, int(n_hosts), _stream(stream))
 
 
 def ring_attn_fwd_host(q_blk, k_all, v_all, o_blk, lse_blk, n_hosts, host_idx, causal, stream=None):

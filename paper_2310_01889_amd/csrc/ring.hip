@@ -16,6 +16,7 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -575,6 +576,60 @@ static RingProblem all_hosts(const void* q, const void* k, const void* v, int B,
 
 using namespace ra;
 
+// ---------------------------------------------------------------------------------
+// Ragged causal lengths.  The sequence is cut into n_hosts blocks of c tokens, c the
+// smallest multiple of 128 with n_hosts * c >= S, so the trailing blocks are short or
+// empty; the tensors are staged into zero-padded workspace copies of length n_hosts * c.
+// Under the causal mask no real query sees a padded key (its position is >= S), and a
+// padded query row adds exactly zero to dK and dV (its o and dO are zero, so Delta = 0,
+// dP = 0 and dS = 0), so the real rows come out as for the unpadded sequence.
+// ---------------------------------------------------------------------------------
+namespace {
+
+__global__ void pad_zero_kernel(uint32_t* base, long long pitch_w, long long off_w, long long len_w,
+                                long long rows) {
+  const long long n = rows * len_w;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x)
+    base[(i / len_w) * pitch_w + off_w + i % len_w] = 0u;
+}
+
+// dst [outer][n_dst units] <- src [outer][n_src units], n_src <= n_dst, the tail of each
+// row zeroed; unit bytes a multiple of 4
+int pad_copy(void* dst, const void* src, long long outer, long long n_src, long long n_dst, long long unit,
+             hipStream_t st) {
+  RA_HIP(hipMemcpy2DAsync(dst, (size_t)(n_dst * unit), src, (size_t)(n_src * unit), (size_t)(n_src * unit),
+                          (size_t)outer, hipMemcpyDeviceToDevice, st));
+  const long long pad_w = (n_dst - n_src) * unit / 4;
+  if (pad_w > 0) {
+    const long long n = outer * pad_w;
+    const int blocks = (int)std::min<long long>((n + 255) / 256, 4096);
+    pad_zero_kernel<<<blocks, 256, 0, st>>>((uint32_t*)dst, n_dst * unit / 4, n_src * unit / 4, pad_w, outer);
+    RA_HIP(hipGetLastError());
+  }
+  return RA_OK;
+}
+
+// dst [outer][n_dst units] <- the first n_dst units of each row of src [outer][n_src units]
+int unpad_copy(void* dst, const void* src, long long outer, long long n_dst, long long n_src, long long unit,
+               hipStream_t st) {
+  RA_HIP(hipMemcpy2DAsync(dst, (size_t)(n_dst * unit), src, (size_t)(n_src * unit), (size_t)(n_dst * unit),
+                          (size_t)outer, hipMemcpyDeviceToDevice, st));
+  return RA_OK;
+}
+
+// *Sp = n_hosts * c
+int padded_len(int S, int N, long long* Sp) {
+  if (S <= 0 || N <= 0) return set_err(RA_EINVAL, "sizes must be positive (S=%d n_hosts=%d)", S, N);
+  const long long c = (((long long)S + N - 1) / N + 127) / 128 * 128;
+  if (c * N > 0x7fffffffll) return set_err(RA_EUNSUPPORTED, "padded length %lld exceeds 2^31-1", c * N);
+  *Sp = c * N;
+  return RA_OK;
+}
+
+}  // namespace
+
+
 extern "C" {
 
 const char* ring_attn_last_error(void) { return g_err.c_str(); }
@@ -696,6 +751,60 @@ int ring_attn_bwd_f32(const float* q, const float* k, const float* v, const floa
   int rc = validate(B, H, S, D, n_hosts, causal, 64);
   if (rc) return rc;
   return run_bwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 4), o, lse, dO, dq, dk, dv, stream);
+}
+
+int ring_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int S,
+                         int D, int n_hosts, hipStream_t stream) {
+  g_err.clear();
+  if (!q || !k || !v || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
+  long long Sp = 0;
+  int rc = padded_len(S, n_hosts, &Sp);
+  if (rc) return rc;
+  rc = validate(B, H, (int)Sp, D, n_hosts, 1, 128);
+  if (rc) return rc;
+  if (Sp == S) return run_fwd(all_hosts(q, k, v, B, H, S, D, n_hosts, 1, 2), o, lse, stream);
+  const long long row = (long long)H * D * 2, t = B * Sp * row;
+  CallResources R(stream);
+  if ((rc = R.alloc((size_t)(4 * t + (long long)B * H * Sp * 4)))) return rc;
+  char* w = (char*)R.ws;
+  char *qp = w, *kp = w + t, *vp = w + 2 * t, *op = w + 3 * t;
+  float* lp = (float*)(w + 4 * t);
+  if ((rc = pad_copy(qp, q, B, S, Sp, row, stream)) || (rc = pad_copy(kp, k, B, S, Sp, row, stream)) ||
+      (rc = pad_copy(vp, v, B, S, Sp, row, stream)))
+    return rc;
+  if ((rc = run_fwd(all_hosts(qp, kp, vp, B, H, (int)Sp, D, n_hosts, 1, 2), op, lp, stream))) return rc;
+  if ((rc = unpad_copy(o, op, B, S, Sp, row, stream))) return rc;
+  return unpad_copy(lse, lp, (long long)B * H, S, Sp, 4, stream);
+}
+
+int ring_attn_bwd_varlen(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                         const void* dO, void* dq, void* dk, void* dv, int B, int H, int S, int D, int n_hosts,
+                         hipStream_t stream) {
+  g_err.clear();
+  if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv) return set_err(RA_EINVAL, "null pointer argument");
+  long long Sp = 0;
+  int rc = padded_len(S, n_hosts, &Sp);
+  if (rc) return rc;
+  rc = validate(B, H, (int)Sp, D, n_hosts, 1, 128);
+  if (rc) return rc;
+  if (Sp == S) return run_bwd(all_hosts(q, k, v, B, H, S, D, n_hosts, 1, 2), o, lse, dO, dq, dk, dv, stream);
+  const long long row = (long long)H * D * 2, t = B * Sp * row;
+  CallResources R(stream);
+  if ((rc = R.alloc((size_t)(8 * t + (long long)B * H * Sp * 4)))) return rc;
+  char* w = (char*)R.ws;
+  char* p[8];
+  for (int i = 0; i < 8; ++i) p[i] = w + i * t;  // q k v o dO dq dk dv
+  float* lp = (float*)(w + 8 * t);
+  const void* src[5] = {q, k, v, o, dO};
+  for (int i = 0; i < 5; ++i)
+    if ((rc = pad_copy(p[i], src[i], B, S, Sp, row, stream))) return rc;
+  if ((rc = pad_copy(lp, lse, (long long)B * H, S, Sp, 4, stream))) return rc;
+  if ((rc = run_bwd(all_hosts(p[0], p[1], p[2], B, H, (int)Sp, D, n_hosts, 1, 2), p[3], lp, p[4], p[5], p[6], p[7],
+                    stream)))
+    return rc;
+  if ((rc = unpad_copy(dq, p[5], B, S, Sp, row, stream)) || (rc = unpad_copy(dk, p[6], B, S, Sp, row, stream)))
+    return rc;
+  return unpad_copy(dv, p[7], B, S, Sp, row, stream);
 }
 
 }  // extern "C"

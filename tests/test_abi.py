@@ -66,6 +66,26 @@ def test_attention_argument_validation(lib):
                              1, 1, 1024, 128, 4, 1, NULL) == RA_EINVAL
 
 
+def test_varlen_argument_validation(lib):
+    """Ragged-length causal entry points: any S >= 1 is accepted in principle; these calls
+    all fail validation, so nothing is allocated or enqueued."""
+    def fwd(*, q=FAKE, B=1, H=1, S=1000, D=128, N=3):
+        return lib.ring_attn_fwd_varlen(q, FAKE, FAKE, FAKE, FAKE, B, H, S, D, N, NULL)
+    assert fwd(q=NULL) == RA_EINVAL
+    assert fwd(S=0) == RA_EINVAL
+    assert fwd(N=0) == RA_EINVAL
+    assert fwd(B=0) == RA_EINVAL
+    assert fwd(D=96) == RA_EUNSUPPORTED
+    assert fwd(N=65) == RA_EUNSUPPORTED
+    assert fwd(S=(1 << 31) - 1, N=64) == RA_EUNSUPPORTED  # padded length above 2^31 - 1
+    assert b"padded length" in lib.ring_attn_last_error()
+    assert fwd(B=1 << 10, H=64, S=(1 << 16) - 5) == RA_EUNSUPPORTED  # padded tensor > 2^31 elements
+    assert lib.ring_attn_bwd_varlen(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, NULL,
+                                    1, 1, 1000, 128, 3, NULL) == RA_EINVAL
+    assert lib.ring_attn_bwd_varlen(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    1, 1, 1000, 96, 3, NULL) == RA_EUNSUPPORTED
+
+
 def test_decode_argument_validation(lib):
     def dec(*, q=FAKE, B=1, H=2, S=4096, D=128, Tq=1, N=8, causal=1):
         return lib.ring_attn_decode(q, FAKE, FAKE, FAKE, FAKE, B, H, S, D, Tq, N, causal, NULL)
