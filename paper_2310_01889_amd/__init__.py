@@ -383,18 +383,30 @@ def llama_stack_train_step(x, layer_params, dz, z, dx, layer_grads, n_heads, n_h
 # Allocating wrappers
 # ----------------------------------------------------------------------------------
 def attention_fwd(q, k, v, n_hosts, causal=True):
-    """Returns (o, lse) for bf16 or float32 q, k, v of shape [B, S, H, D]."""
+    """Returns (o, lse) for bf16 or float32 q, k, v of shape [B, S, H, D].  A bf16 causal
+    sequence whose length does not fill n_hosts blocks of a multiple of 128 tokens goes
+    through ring_attn_fwd_varlen (short or empty last blocks)."""
     B, S, H, D = _bshd(q)
     o = torch.empty_like(q)
     lse = torch.empty((B, H, S), dtype=torch.float32, device=q.device)
+    if _ragged(q, S, n_hosts, causal):
+        ring_attn_fwd_varlen(q, k, v, o, lse, n_hosts)
+        return o, lse
     fn = ring_attn_fwd if q.dtype == torch.bfloat16 else ring_attn_fwd_f32
     fn(q, k, v, o, lse, n_hosts, causal)
     return o, lse
 
 
+def _ragged(q, S, n_hosts, causal):
+    return bool(causal) and q.dtype == torch.bfloat16 and int(n_hosts) > 0 and S % (128 * int(n_hosts)) != 0
+
+
 def attention_bwd(q, k, v, o, lse, dO, n_hosts, causal=True):
-    """Returns (dq, dk, dv)."""
+    """Returns (dq, dk, dv); ragged bf16 causal lengths as in attention_fwd."""
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    if _ragged(q, int(q.shape[1]), n_hosts, causal):
+        ring_attn_bwd_varlen(q, k, v, o, lse, dO, dq, dk, dv, n_hosts)
+        return dq, dk, dv
     fn = ring_attn_bwd if q.dtype == torch.bfloat16 else ring_attn_bwd_f32
     fn(q, k, v, o, lse, dO, dq, dk, dv, n_hosts, causal)
     return dq, dk, dv
