@@ -39,6 +39,13 @@ def _masked_scores(qh, kh, scale, causal, q_pos0, r0):
     return s
 
 
+def _key_end(n_keys, causal, q_offset, r1):
+    """Number of leading keys that can be visible to query rows before r1.  Under the causal
+    mask the keys at positions >= q_offset + r1 are masked for every such row and contribute
+    exactly zero, so they are left out of the row chunk (the same definition, less work)."""
+    return n_keys if not causal else max(0, min(n_keys, q_offset + r1))
+
+
 def attention_fwd(q, k, v, causal, scale=None, q_offset=0, row_chunk=1024):
     """O = softmax(Q K^T * scale) V and lse, per (batch, head).  Returns (o, lse)."""
     q, k, v = _as64(q), _as64(k), _as64(v)
@@ -49,9 +56,10 @@ def attention_fwd(q, k, v, causal, scale=None, q_offset=0, row_chunk=1024):
     lse = np.zeros((B, H, S))
     for b in range(B):
         for h in range(H):
-            kh, vh = k[b, :, h, :], v[b, :, h, :]
             for r0 in range(0, S, row_chunk):
                 r1 = min(S, r0 + row_chunk)
+                ke = _key_end(k.shape[1], causal, q_offset, r1)
+                kh, vh = k[b, :ke, h, :], v[b, :ke, h, :]
                 s = _masked_scores(q[b, r0:r1, h, :], kh, scale, causal, q_offset, r0)
                 m = s.max(axis=1)
                 p = np.exp(s - m[:, None])
@@ -103,9 +111,10 @@ def attention_bwd(q, k, v, do, causal, scale=None, q_offset=0, row_chunk=1024):
     dv = np.zeros_like(v)
     for b in range(B):
         for h in range(H):
-            kh, vh = k[b, :, h, :], v[b, :, h, :]
             for r0 in range(0, S, row_chunk):
                 r1 = min(S, r0 + row_chunk)
+                ke = _key_end(k.shape[1], causal, q_offset, r1)
+                kh, vh = k[b, :ke, h, :], v[b, :ke, h, :]
                 qh, doh = q[b, r0:r1, h, :], do[b, r0:r1, h, :]
                 s = _masked_scores(qh, kh, scale, causal, q_offset, r0)
                 m = s.max(axis=1)
@@ -116,8 +125,8 @@ def attention_bwd(q, k, v, do, causal, scale=None, q_offset=0, row_chunk=1024):
                 dp = doh @ vh.T
                 ds = phat * (dp - delta[:, None])
                 dq[b, r0:r1, h, :] = (ds @ kh) * scale
-                dk[b, :, h, :] += (ds.T @ qh) * scale
-                dv[b, :, h, :] += phat.T @ doh
+                dk[b, :ke, h, :] += (ds.T @ qh) * scale
+                dv[b, :ke, h, :] += phat.T @ doh
     return dq, dk, dv
 
 
@@ -145,3 +154,46 @@ def attention_bwd_rows(q, k, v, do, rows, causal, scale=None, q_offset=0):
             ds = phat * (dos[b, :, h, :] @ vh.T - delta[:, None])
             dq[b, :, h, :] = (ds @ kh) * scale
     return dq
+
+
+def attention_bwd_key_rows(q, k, v, do, key_rows, causal, scale=None, q_offset=0, row_chunk=512):
+    """Rows ``key_rows`` of dk and dv only.  Row s of dk (of dv) sums, over every query row r,
+    the term dS[r, s] q_r / sqrt(d) (Phat[r, s] dO_r), so it needs every query row's
+    normalised probabilities and Delta_r = sum_d dO_rd O_rd: the forward definition is
+    evaluated for all query rows (in row chunks, O recomputed from the definition), and only
+    the columns ``key_rows`` of Phat and dP enter the sums.  Same definition as
+    attention_bwd restricted to those rows.  Returns (dk_rows, dv_rows), each
+    [B, len(key_rows), H, D]; q, k, v, do may be float32 and are upcast one head at a time."""
+    key_rows = np.asarray(key_rows, dtype=np.int64)
+    B, S, H, D = np.shape(q)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    R = len(key_rows)
+    dk = np.zeros((B, R, H, D))
+    dv = np.zeros((B, R, H, np.shape(v)[3]))
+    kpos = key_rows[None, :]
+    for b in range(B):
+        for h in range(H):
+            kh_all, vh_all = k[b, :, h, :], v[b, :, h, :]
+            ks, vs = _as64(kh_all[key_rows]), _as64(vh_all[key_rows])
+            for r0 in range(0, S, row_chunk):
+                r1 = min(S, r0 + row_chunk)
+                ke = _key_end(np.shape(k)[1], causal, q_offset, r1)
+                kh, vh = _as64(kh_all[:ke]), _as64(vh_all[:ke])
+                qh, doh = _as64(q[b, r0:r1, h, :]), _as64(do[b, r0:r1, h, :])
+                s = _masked_scores(qh, kh, scale, causal, q_offset, r0)
+                m = s.max(axis=1)
+                p = np.exp(s - m[:, None])
+                den = p.sum(axis=1)
+                oh = (p @ vh) / den[:, None]
+                delta = (doh * oh).sum(axis=1)
+                # the chosen columns: scores, probabilities and dP against those keys
+                ss = (qh @ ks.T) * scale
+                if causal:
+                    qpos = (q_offset + r0 + np.arange(r1 - r0))[:, None]
+                    ss = np.where(kpos > qpos, -np.inf, ss)
+                phat = np.exp(ss - m[:, None]) / den[:, None]
+                ds = phat * (doh @ vs.T - delta[:, None])
+                dk[b, :, h, :] += (ds.T @ qh) * scale
+                dv[b, :, h, :] += phat.T @ doh
+    return dk, dv

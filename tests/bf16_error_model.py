@@ -123,3 +123,41 @@ def llama_layer_rounding_errors(x, params, dz, n_heads):
         if name in ("z", "dx"):  # magnitude-scaled max, the metric of the z / dx bounds
             out[name + "_scaled_max"] = float((err / np.maximum(1.0, np.abs(r))).max())
     return out
+
+
+def attention_rounding_errors(q, k, v, do, causal=True):
+    """Ring attention forward and backward in exact arithmetic except for what the bf16 path
+    stores in bf16: the probabilities P that multiply V (their row sum, the denominator, is
+    taken over the rounded values), the output o -- which the backward entry point receives
+    in bf16 and which enters Delta = rowsum(dO * o) --, the recomputed P and dS as product
+    operands of the backward, and dq, dk, dv.  Inputs are bf16 tensors [B, S, H, D].
+    Returns, for o and each gradient, (max |err|, max |err| / max(1, |ref|), relative RMS)
+    against the fp64 oracle: the error that bf16 storage alone causes."""
+    from oracle import attention as OA
+
+    B, S, H, D = q.shape
+    Q, K, V, dO = (t.double().permute(0, 2, 1, 3) for t in (q, k, v, do))  # [B, H, S, D]
+    s = Q @ K.transpose(-1, -2) / math.sqrt(D)
+    if causal:
+        s = s.masked_fill(torch.ones(S, S, dtype=torch.bool).triu(1), float("-inf"))
+    m = s.max(-1, keepdim=True).values
+    Pb = _bf(torch.exp(s - m))
+    den = Pb.sum(-1, keepdim=True)
+    o = _bf((Pb @ V) / den)
+    lse = m + torch.log(den)
+    P = torch.exp(s - lse)
+    delta = (dO * o).sum(-1, keepdim=True)
+    dS = _bf(P * (dO @ V.transpose(-1, -2) - delta))
+    dq = _bf(dS @ K / math.sqrt(D))
+    dk = _bf(dS.transpose(-1, -2) @ Q / math.sqrt(D))
+    dv = _bf(_bf(P).transpose(-1, -2) @ dO)
+    f = [t.float().numpy() for t in (q, k, v, do)]
+    o_ref, _ = OA.attention_fwd(*f[:3], causal)
+    refs = (o_ref,) + tuple(OA.attention_bwd(*f, causal))
+    out = {}
+    for name, got, ref in zip(("o", "dq", "dk", "dv"), (o, dq, dk, dv), refs):
+        g = got.permute(0, 2, 1, 3).numpy()
+        err = np.abs(g - ref)
+        out[name] = (float(err.max()), float((err / np.maximum(1.0, np.abs(ref))).max()),
+                     float(np.sqrt((err ** 2).mean() / (ref ** 2).mean())))
+    return out

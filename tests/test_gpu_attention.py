@@ -284,12 +284,14 @@ def test_bf16_forward_large_logits(amp, D):
 def test_bf16_backward_large_logits(D):
     """Backward with scores of standard deviation 4 (queries scaled by 4): the recomputed
     probabilities use float32 scores.  The gradients grow with the scale (|dK| up to ~14
-    here).  An fp64 emulation that rounds to bf16 exactly what this interface and path
-    store in bf16 -- o as the entry point receives it (it enters Delta = rowsum(dO * o)),
-    P and dS as product operands, the outputs -- leaves max errors of 2.3e-2 (dq), 7.8e-2
-    (dk; 7.0e-2 relative to max(1, |ref|)) and 3.5e-3 relative RMS at D = 128 (D = 64: dk
-    5.6e-2 scaled, 3.3e-3 RMS): the bounds are 1e-1 on the magnitude-scaled error and 1e-2
-    relative RMS."""
+    here), and bf16 storage alone -- o as the entry point receives it (it enters
+    Delta = rowsum(dO * o)), P and dS as product operands, the outputs -- leaves a dK error
+    above the plain 5e-2 bound: the CPU emulation of exactly that storage
+    (tests/bf16_error_model.py attention_rounding_errors, checked on its own in
+    tests/test_tolerance_model.py) gives the floor on these same inputs, and each gradient's
+    magnitude-scaled error is bounded by max(5e-2, 1.25 x its floor), its relative RMS by
+    1e-2."""
+    from tests.test_tolerance_model import large_logit_floor
     B, S, H, N = 1, 1024, 2, 4
     q, k, v, do = synth.attention_inputs(13, B, S, H, D, with_grad=True)
     q = q * 4.0
@@ -297,10 +299,13 @@ def test_bf16_backward_large_logits(D):
     o, lse = ra.attention_fwd(qd, kd, vd, N, True)
     dq, dk, dv = ra.attention_bwd(qd, kd, vd, o, lse, dod, N, True)
     torch.cuda.synchronize()
+    floor = large_logit_floor(D)
     ref = OA.attention_bwd(np64(q), np64(k), np64(v), np64(do), True)
     for name, g, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
         e = np.abs(np64(g) - r)
         scaled = float((e / np.maximum(1.0, np.abs(r))).max())
         rms = float(np.sqrt((e ** 2).mean() / (r ** 2).mean()))
-        log("  %s: max|err| %.3e  scaled %.3e  rel rms %.2e  max|ref| %.2f" % (name, e.max(), scaled, rms, np.abs(r).max()))
-        assert scaled <= 1e-1 and rms <= 1e-2
+        bound = max(5e-2, 1.25 * floor[name][1])
+        log("  %s: max|err| %.3e  scaled %.3e (floor %.3e, bound %.3e)  rel rms %.2e  max|ref| %.2f"
+            % (name, e.max(), scaled, floor[name][1], bound, rms, np.abs(r).max()))
+        assert scaled <= bound and rms <= 1e-2

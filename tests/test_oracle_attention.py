@@ -148,3 +148,41 @@ def test_gradient_rows_match_full_backward():
     np.testing.assert_allclose(dqb, dq[:, 24:], atol=1e-13)
     np.testing.assert_allclose(A.attention_bwd_rows(q[:, 24:], k, v, do[:, 24:], [0, 15], True, q_offset=24),
                                dq[:, [24, 39]], atol=1e-13)
+
+
+def _torch_host_share_grads(q, k, v, do, causal, q_offset):
+    """torch fp64 autograd of sum(do * attention(q, k, v)) for a query block at global
+    positions q_offset.. against every key (explicit boolean mask for the offset)."""
+    tq, tk, tv = (torch.from_numpy(x).permute(0, 2, 1, 3).requires_grad_() for x in (q, k, v))
+    mask = None
+    if causal:
+        qpos = q_offset + torch.arange(q.shape[1])[:, None]
+        mask = torch.arange(k.shape[1])[None, :] <= qpos
+    out = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask)
+    out.backward(torch.from_numpy(do).permute(0, 2, 1, 3))
+    return [t.grad.permute(0, 2, 1, 3).numpy() for t in (tq, tk, tv)]
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("q_offset,chunk", [(0, 5), (24, 7), (24, 512)])
+def test_key_row_gradients_match_torch_autograd(causal, q_offset, chunk):
+    """dK / dV rows of chosen keys (the host-share view: a query block at an offset adds its
+    contribution to every key's gradient) against torch autograd, and the host-share
+    backward with its causal key limit against the same."""
+    q, k, v, do = (_rand(s, 2, 40, 2, 8) for s in (37, 38, 39, 40))
+    qb, dob = q[:, q_offset:], do[:, q_offset:]
+    tdq, tdk, tdv = _torch_host_share_grads(qb, k, v, dob, causal, q_offset)
+    rows = np.array([0, 1, 13, 23, 24, 25, 39])
+    dk, dv = A.attention_bwd_key_rows(qb, k, v, dob, rows, causal, q_offset=q_offset, row_chunk=chunk)
+    np.testing.assert_allclose(dk, tdk[:, rows], atol=1e-12)
+    np.testing.assert_allclose(dv, tdv[:, rows], atol=1e-12)
+    dq, dk_all, dv_all = A.attention_bwd(qb, k, v, dob, causal, q_offset=q_offset, row_chunk=chunk)
+    for mine, ref in ((dq, tdq), (dk_all, tdk), (dv_all, tdv)):
+        np.testing.assert_allclose(mine, ref, atol=1e-12)
+    o, lse = A.attention_fwd(qb, k, v, causal, q_offset=q_offset, row_chunk=chunk)
+    tq, tk, tv = (torch.from_numpy(x).permute(0, 2, 1, 3) for x in (qb, k, v))
+    mask = None
+    if causal:
+        mask = torch.arange(40)[None, :] <= (q_offset + torch.arange(qb.shape[1])[:, None])
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask)
+    np.testing.assert_allclose(o, ref.permute(0, 2, 1, 3).numpy(), atol=1e-12)

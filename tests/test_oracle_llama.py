@@ -124,3 +124,62 @@ def test_stack_backward_finite_differences():
     dx1, g1 = L.stack_bwd(x, layers[:1], dz, 2)
     ref = L.layer_bwd(x, *layers[0], dz, 2)
     np.testing.assert_allclose(dx1, ref[0], atol=1e-13)
+
+
+def _torch_llama_layer(x, g1, wq, wk, wv, wo, g2, w1, w3, w2, H, causal=True):
+    """The same pre-norm layer written with torch fp64 library routines: rms_norm, rotary
+    embedding as complex multiplication (torch.polar on interleaved pairs), scaled dot-product
+    attention with its own causal mask, silu."""
+    F = torch.nn.functional
+    S, d = x.shape
+    D = d // H
+    rms = lambda t, g: F.rms_norm(t, (d,), weight=g, eps=L.EPS)
+    inv = L.ROPE_BASE ** (-torch.arange(0, D, 2, dtype=torch.float64) / D)
+    ang = torch.arange(S, dtype=torch.float64)[:, None] * inv[None, :]
+    rot = torch.polar(torch.ones_like(ang), ang)[:, None, :]  # [S, 1, D/2]
+
+    def rope(t):
+        tc = torch.view_as_complex(t.reshape(S, H, D // 2, 2))
+        return torch.view_as_real(tc * rot).reshape(S, d)
+
+    heads = lambda t: t.reshape(S, H, D).transpose(0, 1)
+    n1 = rms(x, g1)
+    a = F.scaled_dot_product_attention(heads(rope(n1 @ wq)), heads(rope(n1 @ wk)), heads(n1 @ wv), is_causal=causal)
+    h = x + a.transpose(0, 1).reshape(S, d) @ wo
+    n2 = rms(h, g2)
+    return h + (F.silu(n2 @ w1) * (n2 @ w3)) @ w2
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_layer_matches_torch_composition(causal):
+    """The layer and its every gradient against the torch restatement and autograd."""
+    params, dz = _tiny_layer(15, S=10, d=16, dff=12)
+    H = 2
+    z = L.layer_fwd(*params, H, causal)
+    ts = [torch.from_numpy(p.copy()).requires_grad_() for p in params]
+    tz = _torch_llama_layer(*ts, H, causal)
+    np.testing.assert_allclose(z, tz.detach().numpy(), atol=1e-12)
+    tz.backward(torch.from_numpy(dz))
+    grads = L.layer_bwd(*params, dz, H, causal)
+    for g, t in zip(grads, ts):  # x, g1, wq, wk, wv, wo, g2, w1, w3, w2
+        np.testing.assert_allclose(g, t.grad.numpy(), atol=1e-11)
+
+
+def test_stack_matches_torch_composition():
+    """A 2-layer stack and its full-recomputation training step against autograd through
+    the torch restatement applied twice."""
+    p1, dz = _tiny_layer(16, S=10, d=16, dff=12)
+    p2, _ = _tiny_layer(17, S=10, d=16, dff=12)
+    x = p1[0]
+    layers = [list(p1[1:]), list(p2[1:])]
+    H = 2
+    tx = torch.from_numpy(x.copy()).requires_grad_()
+    tl = [[torch.from_numpy(p.copy()).requires_grad_() for p in ly] for ly in layers]
+    tz = _torch_llama_layer(_torch_llama_layer(tx, *tl[0], H), *tl[1], H)
+    np.testing.assert_allclose(L.stack_fwd(x, layers, H), tz.detach().numpy(), atol=1e-12)
+    tz.backward(torch.from_numpy(dz))
+    dx, grads = L.stack_bwd(x, layers, dz, H)
+    np.testing.assert_allclose(dx, tx.grad.numpy(), atol=1e-11)
+    for li in range(2):
+        for g, t in zip(grads[li], tl[li]):
+            np.testing.assert_allclose(g, t.grad.numpy(), atol=1e-11)

@@ -138,3 +138,37 @@ def test_llama_swiglu_wrong_derivative_is_caught(monkeypatch):
     import tests.test_oracle_llama as TL
     monkeypatch.setattr(LL, "swiglu_bwd", _mutated(LL, "swiglu_bwd", "w * silu_grad(u)", "w * silu(u)"))
     _fails(TL.test_swiglu_backward_matches_autograd)
+
+
+def test_key_rows_dropped_delta_is_caught(monkeypatch):
+    monkeypatch.setattr(A, "attention_bwd_key_rows",
+                        _mutated(A, "attention_bwd_key_rows", "(doh @ vs.T - delta[:, None])", "(doh @ vs.T)"))
+    _fails(TA.test_key_row_gradients_match_torch_autograd, True, 24, 7)
+
+
+def test_causal_key_limit_one_short_is_caught(monkeypatch):
+    monkeypatch.setattr(A, "_key_end", lambda n, causal, off, r1: n if not causal else max(0, min(n, off + r1 - 1)))
+    _fails(TA.test_naive_matches_torch_sdpa_fp64, True)
+    _fails(TA.test_backward_matches_torch_autograd_fp64, True)
+
+
+def test_llama_composition_slip_in_forward_and_backward_is_caught(monkeypatch):
+    """A wrong rotary base in both the forward and the backward of the layer: the two stay
+    consistent with each other (finite differences pass), so only the torch restatement of
+    the composition can catch it."""
+    from oracle import llama as LL
+    import tests.test_oracle_llama as TL
+    slip = ("eps=EPS, base=ROPE_BASE", "eps=EPS, base=500.0")
+    monkeypatch.setattr(LL, "layer_fwd", _mutated(LL, "layer_fwd", *slip))
+    monkeypatch.setattr(LL, "layer_bwd", _mutated(LL, "layer_bwd", *slip))
+    TL.test_layer_backward_finite_differences(True)  # still self-consistent
+    _fails(TL.test_layer_matches_torch_composition, True)
+    _fails(TL.test_stack_matches_torch_composition)
+
+
+def test_llama_post_norm_residual_is_caught(monkeypatch):
+    """The first residual taken from the normalised input instead of x."""
+    from oracle import llama as LL
+    import tests.test_oracle_llama as TL
+    monkeypatch.setattr(LL, "layer_fwd", _mutated(LL, "layer_fwd", "h = x + a @", "h = n1 + a @"))
+    _fails(TL.test_layer_matches_torch_composition, True)
