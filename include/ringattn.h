@@ -38,7 +38,10 @@
  *     by events, so callers see single-stream semantics.  Distinct streams may be used
  *     from distinct threads concurrently.
  *   - Workspace (receive buffers, float32 accumulators) is allocated stream-ordered on
- *     `stream` and released at the end of the call.
+ *     `stream` from a memory pool the library owns on each device, and freed back to that
+ *     pool at the end of the call (stream-ordered).  The pool keeps freed memory cached for
+ *     later calls until the process ends or ring_attn_release_workspace() is called; the
+ *     device's default memory pool and its settings are not touched.
  *   - Return value: RA_OK or an ra_status error code.  Arguments are validated before
  *     anything is enqueued: on error nothing is enqueued and outputs are untouched.
  *     ring_attn_last_error() describes the last error on the calling thread.  NaN or
@@ -335,6 +338,14 @@ int llama_stack_train_step(const void* x, const void* const* params, const void*
 /* Description of the last error returned on the calling thread ("" if none).  Valid
  * until the next library call on that thread. */
 const char* ring_attn_last_error(void);
+
+/*
+ * Return the cached workspace of the current device's library pool to the driver
+ * (hipMemPoolTrimTo to zero bytes).  Memory still in use by calls whose stream has not
+ * reached the end of the call stays allocated.  Not part of the method.  Returns RA_OK,
+ * or RA_EHIP if the pool cannot be created or trimmed.
+ */
+int ring_attn_release_workspace(void);
 
 /*
  * Kernel timing for benchmarks and profiling (not part of the method).

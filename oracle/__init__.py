@@ -1,6 +1,7 @@
 """CPU oracle for the ring-attention hot path: TEST INFRASTRUCTURE ONLY.
 
-A plain, slow, float64 NumPy implementation of what the HIP library computes, written
+A plain, slow, float64 implementation (NumPy, and plain PyTorch CPU operations where the
+work is large) of what the HIP library computes, written
 from the paper (Liu, Zaharia, Abbeel, "Ring Attention with Blockwise Transformers for
 Near-Infinite Context", arXiv 2310.01889).  Only the test suite, the smoke check in
 ``__graft_entry__.py`` and the ``cpu_baseline`` leg of ``bench.py`` may import it; the

@@ -1,7 +1,8 @@
 """Ring attention with blockwise computation, emulated on the CPU (oracle; test only).
 
 Follows Section 3 ("Ring-Based Blockwise Attention") and the forward/backward code of
-Appendix A, written out with explicit per-host state in float64:
+Appendix A, written out with explicit per-host state in float64 (plain PyTorch CPU
+operations; arguments and results are NumPy arrays):
 
   * The sequence of length S is split into N = n_hosts equal blocks of c = S / N
     tokens; host i owns query block i and, initially, key/value block i.
@@ -26,21 +27,27 @@ to check that the result does not depend on the order in which blocks are folded
 import math
 
 import numpy as np
+import torch
+
+_F64 = torch.float64
 
 
 def _as64(x):
-    return np.asarray(x, dtype=np.float64)
+    """float64 CPU tensor of an array-like (NumPy array or torch tensor)."""
+    if torch.is_tensor(x):
+        return x.detach().to(device="cpu", dtype=_F64)
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(x, dtype=np.float64)))
 
 
 def _scores(qc, kc, scale):
     """[B, cq, H, D] x [B, ck, H, D] -> [B, H, cq, ck]."""
-    return np.einsum("bqhd,bkhd->bhqk", qc, kc) * scale
+    return torch.einsum("bqhd,bkhd->bhqk", qc, kc) * scale
 
 
 def _visible(q_pos, k_pos, causal):
     """Boolean [cq, ck]: key k_pos[j] is visible to query q_pos[i]."""
     if not causal:
-        return np.ones((len(q_pos), len(k_pos)), dtype=bool)
+        return torch.ones((len(q_pos), len(k_pos)), dtype=torch.bool)
     return k_pos[None, :] <= q_pos[:, None]
 
 
@@ -50,24 +57,24 @@ def _fold_block_fwd(state, q, kblk, vblk, q_pos0, k_pos0, causal, scale, qchunk,
     c_q, c_k = q.shape[1], kblk.shape[1]
     for q0 in range(0, c_q, qchunk):
         q1 = min(c_q, q0 + qchunk)
-        q_pos = q_pos0 + np.arange(q0, q1)
+        q_pos = q_pos0 + torch.arange(q0, q1)
         for k0 in range(0, c_k, kchunk):
             k1 = min(c_k, k0 + kchunk)
-            k_pos = k_pos0 + np.arange(k0, k1)
+            k_pos = k_pos0 + torch.arange(k0, k1)
             vis = _visible(q_pos, k_pos, causal)
-            if not vis.any():
+            if not bool(vis.any()):
                 continue  # fully masked tile: contributes nothing
             s = _scores(q[:, q0:q1], kblk[:, k0:k1], scale)
-            s = np.where(vis[None, None], s, -np.inf)
+            s = s.masked_fill(~vis[None, None], float("-inf"))
             m_old = mx[:, :, q0:q1]
-            m_new = np.maximum(m_old, s.max(axis=3))
+            m_new = torch.maximum(m_old, s.amax(dim=3))
             # rows with no visible key so far keep m = -inf; shift by 0 there
-            m_safe = np.where(np.isneginf(m_new), 0.0, m_new)
-            p = np.exp(s - m_safe[..., None])  # masked -> exp(-inf) = 0
-            corr = np.exp(m_old - m_safe)      # m_old = -inf -> 0
-            den[:, :, q0:q1] = den[:, :, q0:q1] * corr + p.sum(axis=3)
-            corr_o = np.transpose(corr, (0, 2, 1))[..., None]  # [B, cq, H, 1]
-            pv = np.einsum("bhqk,bkhd->bqhd", p, vblk[:, k0:k1])
+            m_safe = torch.where(torch.isneginf(m_new), torch.zeros_like(m_new), m_new)
+            p = torch.exp(s - m_safe[..., None])  # masked -> exp(-inf) = 0
+            corr = torch.exp(m_old - m_safe)      # m_old = -inf -> 0
+            den[:, :, q0:q1] = den[:, :, q0:q1] * corr + p.sum(dim=3)
+            corr_o = corr.permute(0, 2, 1)[..., None]  # [B, cq, H, 1]
+            pv = torch.einsum("bhqk,bkhd->bqhd", p, vblk[:, k0:k1])
             num[:, q0:q1] = num[:, q0:q1] * corr_o + pv
             mx[:, :, q0:q1] = m_new
 
@@ -80,7 +87,12 @@ def ring_attention_fwd(q, k, v, n_hosts, causal, query_chunk=None, key_chunk=Non
     ``order[i][t]`` (optional) is the block host i folds in at step t; without it the
     blocks are rotated around the ring.
     """
-    q, k, v = _as64(q), _as64(k), _as64(v)
+    o, lse, mx, den = _ring_fwd(_as64(q), _as64(k), _as64(v), n_hosts, causal, query_chunk, key_chunk, order,
+                                scale)
+    return o.numpy(), lse.numpy(), mx.numpy(), den.numpy()
+
+
+def _ring_fwd(q, k, v, n_hosts, causal, query_chunk, key_chunk, order, scale):
     B, S, H, D = q.shape
     N = int(n_hosts)
     if S % N:
@@ -92,9 +104,9 @@ def ring_attention_fwd(q, k, v, n_hosts, causal, query_chunk=None, key_chunk=Non
         scale = 1.0 / math.sqrt(D)
     blk = lambda x, j: x[:, j * c:(j + 1) * c]
     # per-host state: the initial carry of the paper (max = -inf, zeros elsewhere)
-    mx = [np.full((B, H, c), -np.inf) for _ in range(N)]
-    num = [np.zeros((B, c, H, D)) for _ in range(N)]
-    den = [np.zeros((B, H, c)) for _ in range(N)]
+    mx = [torch.full((B, H, c), float("-inf"), dtype=_F64) for _ in range(N)]
+    num = [torch.zeros((B, c, H, D), dtype=_F64) for _ in range(N)]
+    den = [torch.zeros((B, H, c), dtype=_F64) for _ in range(N)]
     # what each host currently holds: (block index, k block, v block)
     held = [(i, blk(k, i), blk(v, i)) for i in range(N)]
     for t in range(N):
@@ -108,10 +120,10 @@ def ring_attention_fwd(q, k, v, n_hosts, causal, query_chunk=None, key_chunk=Non
                             i * c, j * c, causal, scale, qchunk, kchunk)
         # ppermute: host i sends what it holds to host i+1 (receives from i-1)
         held = [held[(i - 1) % N] for i in range(N)]
-    o = np.concatenate([num[i] / np.transpose(den[i], (0, 2, 1))[..., None] for i in range(N)], axis=1)
-    mx_all = np.concatenate(mx, axis=2)
-    den_all = np.concatenate(den, axis=2)
-    lse = mx_all + np.log(den_all)
+    o = torch.cat([num[i] / den[i].permute(0, 2, 1)[..., None] for i in range(N)], dim=1)
+    mx_all = torch.cat(mx, dim=2)
+    den_all = torch.cat(den, dim=2)
+    lse = mx_all + torch.log(den_all)
     return o, lse, mx_all, den_all
 
 
@@ -119,32 +131,32 @@ def _fold_block_bwd(q, kblk, vblk, o, do, lse, dq, dkblk, dvblk, q_pos0, k_pos0,
                     scale, qchunk, kchunk):
     """Add one key/value block's contributions to dq (local) and dk, dv (travelling)."""
     c_q, c_k = q.shape[1], kblk.shape[1]
-    delta = np.transpose((do * o).sum(axis=3), (0, 2, 1))  # [B, H, c_q]
+    delta = (do * o).sum(dim=3).permute(0, 2, 1)  # [B, H, c_q]
     for q0 in range(0, c_q, qchunk):
         q1 = min(c_q, q0 + qchunk)
-        q_pos = q_pos0 + np.arange(q0, q1)
+        q_pos = q_pos0 + torch.arange(q0, q1)
         for k0 in range(0, c_k, kchunk):
             k1 = min(c_k, k0 + kchunk)
-            k_pos = k_pos0 + np.arange(k0, k1)
+            k_pos = k_pos0 + torch.arange(k0, k1)
             vis = _visible(q_pos, k_pos, causal)
-            if not vis.any():
+            if not bool(vis.any()):
                 continue
             s = _scores(q[:, q0:q1], kblk[:, k0:k1], scale)
             # normalised probabilities straight from the saved log-sum-exp
-            p = np.where(vis[None, None], np.exp(s - lse[:, :, q0:q1, None]), 0.0)
-            dvblk[:, k0:k1] += np.einsum("bhqk,bqhd->bkhd", p, do[:, q0:q1])
-            dp = np.einsum("bqhd,bkhd->bhqk", do[:, q0:q1], vblk[:, k0:k1])
+            p = torch.exp(s - lse[:, :, q0:q1, None]).masked_fill(~vis[None, None], 0.0)
+            dvblk[:, k0:k1] += torch.einsum("bhqk,bqhd->bkhd", p, do[:, q0:q1])
+            dp = torch.einsum("bqhd,bkhd->bhqk", do[:, q0:q1], vblk[:, k0:k1])
             ds = p * (dp - delta[:, :, q0:q1, None])
-            dq[:, q0:q1] += np.einsum("bhqk,bkhd->bqhd", ds, kblk[:, k0:k1]) * scale
-            dkblk[:, k0:k1] += np.einsum("bhqk,bqhd->bkhd", ds, q[:, q0:q1]) * scale
+            dq[:, q0:q1] += torch.einsum("bhqk,bkhd->bqhd", ds, kblk[:, k0:k1]) * scale
+            dkblk[:, k0:k1] += torch.einsum("bhqk,bqhd->bkhd", ds, q[:, q0:q1]) * scale
 
 
 def ring_attention_bwd(q, k, v, do, n_hosts, causal, query_chunk=None, key_chunk=None,
                        order=None, scale=None):
     """Gradients (dq, dk, dv) of sum(do * O) through the ring.
 
-    The forward output and log-sum-exp used as residuals are recomputed here with
-    ``ring_attention_fwd`` (the paper's residuals are output, denominator and max;
+    The forward output and log-sum-exp used as residuals are recomputed here with the
+    ring forward (the paper's residuals are output, denominator and max;
     lse = max + ln(denominator) carries the same information).
     """
     q, k, v, do = _as64(q), _as64(k), _as64(v), _as64(do)
@@ -155,14 +167,14 @@ def ring_attention_bwd(q, k, v, do, n_hosts, causal, query_chunk=None, key_chunk
     kchunk = c if key_chunk is None else int(key_chunk)
     if scale is None:
         scale = 1.0 / math.sqrt(D)
-    o, lse, _, _ = ring_attention_fwd(q, k, v, N, causal, qchunk, kchunk, order, scale)
+    o, lse, _, _ = _ring_fwd(q, k, v, N, causal, qchunk, kchunk, order, scale)
     blk = lambda x, j: x[:, j * c:(j + 1) * c]
     lse_blk = lambda j: lse[:, :, j * c:(j + 1) * c]
-    dq = [np.zeros((B, c, H, D)) for _ in range(N)]
+    zeros = lambda: torch.zeros((B, c, H, D), dtype=_F64)
+    dq = [zeros() for _ in range(N)]
     if order is None:
         # (block index, k, v, dk, dv) travel together around the ring
-        held = [(i, blk(k, i), blk(v, i), np.zeros((B, c, H, D)), np.zeros((B, c, H, D)))
-                for i in range(N)]
+        held = [(i, blk(k, i), blk(v, i), zeros(), zeros()) for i in range(N)]
         for t in range(N):
             for i in range(N):
                 j, kb, vb, dkb, dvb = held[i]
@@ -171,26 +183,28 @@ def ring_attention_bwd(q, k, v, do, n_hosts, causal, query_chunk=None, key_chunk
             held = [held[(i - 1) % N] for i in range(N)]
         # after N rotations every block is back at its home host
         assert all(held[i][0] == i for i in range(N))
-        dk = np.concatenate([held[i][3] for i in range(N)], axis=1)
-        dv = np.concatenate([held[i][4] for i in range(N)], axis=1)
+        dk = torch.cat([held[i][3] for i in range(N)], dim=1)
+        dv = torch.cat([held[i][4] for i in range(N)], dim=1)
     else:
-        dkb = [np.zeros((B, c, H, D)) for _ in range(N)]
-        dvb = [np.zeros((B, c, H, D)) for _ in range(N)]
+        dkb = [zeros() for _ in range(N)]
+        dvb = [zeros() for _ in range(N)]
         for t in range(N):
             for i in range(N):
                 j = int(order[i][t])
                 _fold_block_bwd(blk(q, i), blk(k, j), blk(v, j), blk(o, i), blk(do, i),
                                 lse_blk(i), dq[i], dkb[j], dvb[j], i * c, j * c, causal,
                                 scale, qchunk, kchunk)
-        dk = np.concatenate(dkb, axis=1)
-        dv = np.concatenate(dvb, axis=1)
-    return np.concatenate(dq, axis=1), dk, dv
+        dk = torch.cat(dkb, dim=1)
+        dv = torch.cat(dvb, dim=1)
+    return torch.cat(dq, dim=1).numpy(), dk.numpy(), dv.numpy()
 
 
 def ring_host_fwd(q_blk, k, v, n_hosts, host_idx, causal, query_chunk=None,
-                  key_chunk=None, scale=None):
+                  key_chunk=None, scale=None, blocks=None):
     """One host's share: query block ``host_idx`` against all N key/value blocks, in
-    the order they reach that host around the ring ((host_idx - t) mod N).
+    the order they reach that host around the ring ((host_idx - t) mod N).  ``blocks``
+    (optional) limits the fold to the first ``blocks`` steps of that order (a partial
+    state, used to time a bounded part of the work).
 
     Returns (o_blk [B,c,H,D], lse_blk [B,H,c]).
     """
@@ -204,11 +218,12 @@ def ring_host_fwd(q_blk, k, v, n_hosts, host_idx, causal, query_chunk=None,
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     i = int(host_idx)
-    state = (np.full((B, H, c), -np.inf), np.zeros((B, c, H, D)), np.zeros((B, H, c)))
-    for t in range(N):
+    state = (torch.full((B, H, c), float("-inf"), dtype=_F64), torch.zeros((B, c, H, D), dtype=_F64),
+             torch.zeros((B, H, c), dtype=_F64))
+    for t in range(N if blocks is None else int(blocks)):
         j = (i - t) % N
         _fold_block_fwd(state, q_blk, k[:, j * c:(j + 1) * c], v[:, j * c:(j + 1) * c],
                         i * c, j * c, causal, scale, qchunk, kchunk)
     mx, num, den = state
-    o = num / np.transpose(den, (0, 2, 1))[..., None]
-    return o, mx + np.log(den)
+    o = num / den.permute(0, 2, 1)[..., None]
+    return o.numpy(), (mx + torch.log(den)).numpy()

@@ -35,6 +35,7 @@ _P = ctypes.c_void_p
 _I = ctypes.c_int
 _SIGS = {
     "ring_attn_mfma_probe": [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p],
+    "ring_attn_release_workspace": [],
     "ring_attn_fwd": [_P] * 5 + [_I] * 6 + [_P],
     "ring_attn_fwd_f32": [_P] * 5 + [_I] * 6 + [_P],
     "ring_attn_bwd": [_P] * 9 + [_I] * 6 + [_P],
@@ -122,6 +123,11 @@ def timing_read(kind):
     if rc != 0:
         raise RingAttnError("ring_attn_timing_read", rc, lib.ring_attn_last_error().decode())
     return ms.value, n.value
+
+
+def release_workspace():
+    """Return the library's cached workspace on the current device to the driver."""
+    _call("ring_attn_release_workspace")
 
 
 MFMA_PROBE_WAVES = 2048

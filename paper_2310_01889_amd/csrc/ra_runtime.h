@@ -22,22 +22,44 @@ int set_err(int code, const char* fmt, ...);
                      #expr, hipGetErrorString(e_));                                    \
   } while (0)
 
-void keep_pool();
+// The current device's workspace pool: a stream-ordered memory pool owned by the library
+// (created on first use, release threshold unlimited, so workspace freed at the end of a
+// call is reused by the next call instead of being unmapped and mapped again).  The
+// device's default pool is left as it is.
+int workspace_pool(hipMemPool_t* out);
 
 // Stream-ordered workspace and events owned by one call; released on every exit path.
+// side: the library's side stream when the call enqueued work on it.  Before the workspace
+// goes back to the pool the caller stream waits for everything enqueued on the side stream
+// so far -- also on an error return in the middle of a call, where the call's own final
+// join was never enqueued -- so that no copy still queued there can write into memory a
+// later call has been given.
 struct CallResources {
   hipStream_t stream;
+  hipStream_t side = nullptr;
   void* ws = nullptr;
   std::vector<hipEvent_t> events;
   explicit CallResources(hipStream_t s) : stream(s) {}
   ~CallResources() {
+    if (ws && side && side != stream) {
+      hipEvent_t e;
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) == hipSuccess) {
+        (void)hipEventRecord(e, side);
+        (void)hipStreamWaitEvent(stream, e, 0);
+        (void)hipEventDestroy(e);
+      } else {
+        (void)hipStreamSynchronize(side);
+      }
+    }
     if (ws) (void)hipFreeAsync(ws, stream);
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
   }
   int alloc(size_t bytes) {
     if (bytes == 0) return RA_OK;
-    keep_pool();
-    RA_HIP(hipMallocAsync(&ws, bytes, stream));
+    hipMemPool_t pool;
+    int rc = workspace_pool(&pool);
+    if (rc) return rc;
+    RA_HIP(hipMallocFromPoolAsync(&ws, bytes, pool, stream));
     return RA_OK;
   }
   int event(hipEvent_t* e) {

@@ -60,23 +60,32 @@ int side_stream(hipStream_t* out) {
 }
 
 namespace {
-bool g_pool_kept[64];
+hipMemPool_t g_pool[64];
 }  // namespace
 
-// Keep the current device's stream-ordered allocations cached in its default pool between
-// calls (release threshold: unlimited).  Otherwise the workspace freed at the end of a call
-// goes back to the driver at the next synchronisation and the next call maps it again.
-void keep_pool() {
+int workspace_pool(hipMemPool_t* out) {
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+  RA_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return set_err(RA_EHIP, "device index %d out of range", dev);
   std::lock_guard<std::mutex> lk(g_mu);
-  if (g_pool_kept[dev]) return;
-  hipMemPool_t pool;
-  if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+  if (!g_pool[dev]) {
+    hipMemPoolProps props{};
+    props.allocType = hipMemAllocationTypePinned;
+    props.handleTypes = hipMemHandleTypeNone;
+    props.location.type = hipMemLocationTypeDevice;
+    props.location.id = dev;
+    hipMemPool_t pool;
+    RA_HIP(hipMemPoolCreate(&pool, &props));
     uint64_t thr = ~0ull;
-    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+    hipError_t e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+    if (e != hipSuccess) {
+      (void)hipMemPoolDestroy(pool);
+      return set_err(RA_EHIP, "hipMemPoolSetAttribute failed: %s", hipGetErrorString(e));
+    }
+    g_pool[dev] = pool;
   }
-  g_pool_kept[dev] = true;
+  *out = g_pool[dev];
+  return RA_OK;
 }
 
 // ---------------------------------------------------------------------------------
@@ -181,6 +190,7 @@ static int run_ring(const RingProblem& P, hipStream_t stream, CallResources& R, 
   if (!serial && !forward && N > 1) {
     int rc = side_stream(&side);
     if (rc) return rc;
+    R.side = side;
   }
   std::vector<hipEvent_t> ev_copy(N + 1, nullptr);
   hipEvent_t ev_entry = nullptr;
@@ -462,6 +472,7 @@ static int run_bwd_host(const void* q_blk, const void* k_all, const void* v_all,
   hipStream_t side = stream;
   rc = side_stream(&side);
   if (rc) return rc;
+  R.side = side;
   hipEvent_t ev;
   if ((rc = R.event(&ev))) return rc;
   RA_HIP(hipEventRecord(ev, stream));
@@ -633,6 +644,15 @@ int padded_len(int S, int N, long long* Sp) {
 extern "C" {
 
 const char* ring_attn_last_error(void) { return g_err.c_str(); }
+
+int ring_attn_release_workspace(void) {
+  g_err.clear();
+  hipMemPool_t pool;
+  int rc = workspace_pool(&pool);
+  if (rc) return rc;
+  RA_HIP(hipMemPoolTrimTo(pool, 0));
+  return RA_OK;
+}
 
 void ring_attn_timing_enable(int on) {
   std::lock_guard<std::mutex> lk(g_tmu);

@@ -309,3 +309,15 @@ def test_bf16_backward_large_logits(D):
         log("  %s: max|err| %.3e  scaled %.3e (floor %.3e, bound %.3e)  rel rms %.2e  max|ref| %.2f"
             % (name, e.max(), scaled, floor[name][1], bound, rms, np.abs(r).max()))
         assert scaled <= bound and rms <= 1e-2
+
+
+def test_release_workspace_between_calls():
+    """The library pool's cached workspace can be returned to the driver between calls; the
+    next call allocates afresh and gives the same result."""
+    q, k, v = dev(*synth.attention_inputs(14, 1, 1024, 2, 128))
+    o1, l1 = ra.attention_fwd(q, k, v, 4, True)
+    torch.cuda.synchronize()
+    ra.release_workspace()
+    o2, l2 = ra.attention_fwd(q, k, v, 4, True)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)

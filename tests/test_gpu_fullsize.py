@@ -17,29 +17,66 @@ pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 TOL_O, TOL_G = 2e-2, 5e-2
 
 
-def f32(t):
-    """float32 NumPy view of a bf16 tensor (exact); the oracle upcasts one head at a time."""
-    return t.float().numpy()
-
-
 def _sample_rows(n, c, extra):
     rng = np.random.default_rng(n)
     rows = set(extra) | set(rng.integers(0, c, size=n).tolist())
     return np.array(sorted(rows))
 
 
+def _tile_rows(n_rows, tile, seed, extra=()):
+    """One row per tile of ``tile`` rows (a random offset in each), plus ``extra`` rows."""
+    rng = np.random.default_rng(seed)
+    rows = np.arange(0, n_rows, tile) + rng.integers(0, tile, size=n_rows // tile)
+    return np.array(sorted(set(rows.tolist()) | set(extra)))
+
+
 def test_causal_forward_S32768_H32_hosts8():
+    """The forward's work items are (host, head, 128-row query tile): one sampled row of every
+    query tile of every head is compared (8192 rows), plus the block edges."""
     B, S, H, D, N = 1, 32768, 32, 128, 8
     q, k, v = synth.attention_inputs(2, B, S, H, D)
     o, lse = ra.attention_fwd(*dev(q, k, v), N, True)
     torch.cuda.synchronize()
+    o, lse = o.cpu(), lse.cpu()
     c = S // N
-    rows = _sample_rows(48, S, [0, 1, c - 1, c, 3 * c + 17, S - c, S - 1])
-    o_ref, lse_ref = OA.attention_rows(f32(q), f32(k), f32(v), rows, True)
-    idx = torch.from_numpy(rows).cuda()
-    eo, el = max_err(o[:, idx], o_ref), max_err(lse[:, :, idx], lse_ref)
-    log("   C2 sampled rows: o %.3e lse %.3e" % (eo, el))
-    assert eo <= TOL_O and el <= TOL_O
+    worst = [0.0, 0.0]
+    for h in range(H):
+        rows = _tile_rows(S, 128, 200 + h, [0, 1, c - 1, c, 3 * c + 17, S - c, S - 1])
+        hs = slice(h, h + 1)
+        o_ref, lse_ref = OA.attention_rows(q[:, :, hs], k[:, :, hs], v[:, :, hs], rows, True)
+        worst[0] = max(worst[0], max_err(o[:, rows, hs], o_ref))
+        worst[1] = max(worst[1], max_err(lse[:, hs][:, :, rows], lse_ref))
+    log("   C2, one row per query tile of every head: o %.3e lse %.3e" % tuple(worst))
+    assert worst[0] <= TOL_O and worst[1] <= TOL_O
+
+
+def test_causal_backward_S65536_H2_hosts8_c8192():
+    """The attention of the Algorithm 1 layer at its ring shape (S = 65536 in 8 blocks of
+    8192), forward and backward through ring_attn_fwd / ring_attn_bwd: head 0 compared in
+    full (o, lse, dq, dk, dv), head 1 on one sampled query row per tile (o, lse, dq)."""
+    B, S, H, D, N = 1, 65536, 2, 128, 8
+    q, k, v, do = synth.attention_inputs(44, B, S, H, D, with_grad=True)
+    qd, kd, vd, dod = dev(q, k, v, do)
+    o, lse = ra.attention_fwd(qd, kd, vd, N, True)
+    dq, dk, dv = ra.attention_bwd(qd, kd, vd, o, lse, dod, N, True)
+    torch.cuda.synchronize()
+    o, lse, dq, dk, dv = (t.cpu() for t in (o, lse, dq, dk, dv))
+    del qd, kd, vd, dod
+    h0 = slice(0, 1)
+    o_ref, lse_ref = OA.attention_fwd(q[:, :, h0], k[:, :, h0], v[:, :, h0], True)
+    eo, el = max_err(o[:, :, h0], o_ref), max_err(lse[:, h0], lse_ref)
+    log("   head 0 forward: o %.3e lse %.3e" % (eo, el))
+    g_ref = OA.attention_bwd(q[:, :, h0], k[:, :, h0], v[:, :, h0], do[:, :, h0], True)
+    eg = [max_err(t[:, :, h0], r) for t, r in zip((dq, dk, dv), g_ref)]
+    log("   head 0 backward: dq %.3e dk %.3e dv %.3e" % tuple(eg))
+    assert eo <= TOL_O and el <= TOL_O and max(eg) <= TOL_G
+    h1 = slice(1, 2)
+    rows = _tile_rows(S, 128, 45, [0, S // N - 1, S // N, S - 1])
+    o_ref, lse_ref = OA.attention_rows(q[:, :, h1], k[:, :, h1], v[:, :, h1], rows, True)
+    dq_ref = OA.attention_bwd_rows(q[:, :, h1], k[:, :, h1], v[:, :, h1], do[:, :, h1], rows, True)
+    e1 = (max_err(o[:, rows, h1], o_ref), max_err(lse[:, h1][:, :, rows], lse_ref), max_err(dq[:, rows, h1], dq_ref))
+    log("   head 1 sampled rows: o %.3e lse %.3e dq %.3e" % e1)
+    assert e1[0] <= TOL_O and e1[1] <= TOL_O and e1[2] <= TOL_G
 
 
 def _host_inputs(seed, B, c, H, D, N, host):
@@ -47,11 +84,15 @@ def _host_inputs(seed, B, c, H, D, N, host):
     return q, k, v, do
 
 
-def test_one_host_share_forward_backward_c32768_hosts8():
+@pytest.fixture(scope="module")
+def host7():
     """Host 7 of 8: a 32768-token query block against 262144 keys, forward, then the
-    backward with dK/dV travelling through the double buffer."""
+    backward with dK/dV travelling through the double buffer (accumulators start at zero,
+    so they hold this host's contributions).  Results are copied to the host; dK/dV of
+    head 0 only, plus their sums over the keys for every head."""
     B, c, H, D, N, host = 1, 32768, 32, 128, 8, 7
     S = N * c
+    log("host-share case: B=%d c=%d H=%d D=%d n_hosts=%d host=%d" % (B, c, H, D, N, host))
     q, k, v, do = _host_inputs(5, B, c, H, D, N, host)
     qd, kd, vd, dod = dev(q, k, v, do)
     o = torch.empty_like(qd)
@@ -62,23 +103,81 @@ def test_one_host_share_forward_backward_c32768_hosts8():
     dv_acc = torch.zeros_like(dk_acc)
     ra.ring_attn_bwd_host(qd, kd, vd, o, lse, dod, dq, dk_acc, dv_acc, N, host, True)
     torch.cuda.synchronize()
-    rows = _sample_rows(24, c, [0, 1, 4095, c - 1])
-    idx = torch.from_numpy(rows).cuda()
-    qf, kf, vf, dof = f32(q), f32(k), f32(v), f32(do)
-    o_ref, lse_ref = OA.attention_rows(qf, kf, vf, rows, True, q_offset=host * c)
-    eo, el = max_err(o[:, idx], o_ref), max_err(lse[:, :, idx], lse_ref)
-    dq_ref = OA.attention_bwd_rows(qf, kf, vf, dof, rows, True, q_offset=host * c)
-    eq = max_err(dq[:, idx], dq_ref)
-    log("   host 7 sampled rows: o %.3e lse %.3e dq %.3e" % (eo, el, eq))
-    assert eo <= TOL_O and el <= TOL_O and eq <= TOL_G
-    # the contributions of one host's queries to dK sum to zero over the keys and those
-    # to dV sum to the host's upstream gradient (rows of dS sum to zero; rows of P to one)
-    sk = dk_acc.sum(dim=1).double().cpu().numpy()
-    sv = dv_acc.sum(dim=1).double().cpu().numpy()
-    ref_sv = np64(do).sum(axis=1)
-    log("   sum dK %.3e  sum dV - sum dO %.3e (scale %.1f)" % (np.abs(sk).max(), np.abs(sv - ref_sv).max(),
-                                                            np.abs(ref_sv).max()))
-    assert np.abs(sk).max() <= 1.0 and np.abs(sv - ref_sv).max() <= 1.0
+    out = dict(q=q, k=k, v=v, do=do, o=o.cpu(), lse=lse.cpu(), dq=dq.cpu(),
+               dk0=dk_acc[:, :, 0:1].cpu(), dv0=dv_acc[:, :, 0:1].cpu(),
+               sk=dk_acc.sum(dim=1).double().cpu().numpy(), sv=dv_acc.sum(dim=1).double().cpu().numpy(),
+               c=c, H=H, N=N, host=host)
+    del qd, kd, vd, dod, dk_acc, dv_acc
+    torch.cuda.empty_cache()
+    return out
+
+
+def test_host_share_forward_rows_c32768_hosts8(host7):
+    """One sampled query row of each of the 256 query tiles, in every head, plus rows 0 and
+    c - 1: o and lse against the oracle on those rows (global positions 7c + r)."""
+    t = host7
+    c, off = t["c"], t["host"] * t["c"]
+    worst = [0.0, 0.0]
+    for h in range(t["H"]):
+        rows = _tile_rows(c, 128, 300 + h, [0, 1, c - 1])
+        hs = slice(h, h + 1)
+        o_ref, lse_ref = OA.attention_rows(t["q"][:, :, hs], t["k"][:, :, hs], t["v"][:, :, hs], rows, True,
+                                           q_offset=off)
+        worst[0] = max(worst[0], max_err(t["o"][:, rows, hs], o_ref))
+        worst[1] = max(worst[1], max_err(t["lse"][:, hs][:, :, rows], lse_ref))
+    log("   host 7, one row per query tile of every head: o %.3e lse %.3e" % tuple(worst))
+    assert worst[0] <= TOL_O and worst[1] <= TOL_O
+
+
+def test_host_share_dq_rows_c32768_hosts8(host7):
+    """dq on one sampled query row of each query tile, in every head, plus rows 0, c - 1."""
+    t = host7
+    c, off = t["c"], t["host"] * t["c"]
+    worst = 0.0
+    for h in range(t["H"]):
+        rows = _tile_rows(c, 128, 400 + h, [0, 1, c - 1])
+        hs = slice(h, h + 1)
+        dq_ref = OA.attention_bwd_rows(t["q"][:, :, hs], t["k"][:, :, hs], t["v"][:, :, hs], t["do"][:, :, hs],
+                                       rows, True, q_offset=off)
+        worst = max(worst, max_err(t["dq"][:, rows, hs], dq_ref))
+    log("   host 7, one dq row per query tile of every head: %.3e" % worst)
+    assert worst <= TOL_G
+
+
+def test_host_share_dkdv_key_rows_c32768_hosts8(host7):
+    """This host's contributions to dK and dV, element by element, on 32 sampled key rows of
+    each of the 8 blocks (edges included) of head 0: the oracle evaluates the host's 32768
+    query rows in full to get every row's probabilities and Delta."""
+    t = host7
+    c, N, off = t["c"], t["N"], t["host"] * t["c"]
+    rng = np.random.default_rng(7)
+    rows = sorted(set(j * c + r for j in range(N)
+                      for r in [0, 1, c // 2, c - 1] + rng.integers(0, c, size=28).tolist()))
+    rows = np.array(rows)
+    h0 = slice(0, 1)
+    # the contributions are sums over query rows: evaluated in slices of 4096 query rows
+    dk_ref, dv_ref = 0.0, 0.0
+    for r0 in range(0, c, 4096):
+        qs = slice(r0, r0 + 4096)
+        dk_s, dv_s = OA.attention_bwd_key_rows(t["q"][:, qs, h0], t["k"][:, :, h0], t["v"][:, :, h0],
+                                               t["do"][:, qs, h0], rows, True, q_offset=off + r0)
+        dk_ref, dv_ref = dk_ref + dk_s, dv_ref + dv_s
+        log("     query rows %d..%d done" % (r0, r0 + 4095))
+    ek, ev = max_err(t["dk0"][:, rows], dk_ref), max_err(t["dv0"][:, rows], dv_ref)
+    log("   host 7, %d key rows of head 0: dk %.3e dv %.3e (max |ref| %.3e / %.3e)"
+        % (len(rows), ek, ev, np.abs(dk_ref).max(), np.abs(dv_ref).max()))
+    assert ek <= TOL_G and ev <= TOL_G
+
+
+def test_host_share_gradient_sums_c32768_hosts8(host7):
+    """The contributions of one host's queries to dK sum to zero over the keys and those to
+    dV sum to the host's upstream gradient (rows of dS sum to zero; rows of P to one), in
+    every head."""
+    t = host7
+    ref_sv = np64(t["do"]).sum(axis=1)
+    ek, ev = np.abs(t["sk"]).max(), np.abs(t["sv"] - ref_sv).max()
+    log("   sum dK %.3e  sum dV - sum dO %.3e (scale %.1f)" % (ek, ev, np.abs(ref_sv).max()))
+    assert ek <= 1.0 and ev <= 1.0
 
 
 @pytest.mark.parametrize("host", [0, 3, 7])

@@ -28,18 +28,20 @@ def test_dropped_scale_is_caught(monkeypatch):
 
 
 def test_off_by_one_causal_mask_is_caught(monkeypatch):
+    import torch
+
     def masked(qh, kh, scale, causal, q_pos0, r0):
         s = (qh @ kh.T) * scale
-        qpos = q_pos0 + r0 + np.arange(qh.shape[0])[:, None]
-        kpos = np.arange(kh.shape[0])[None, :]
-        return np.where(kpos > qpos + 1, -np.inf, s) if causal else s
+        qpos = q_pos0 + r0 + torch.arange(qh.shape[0])[:, None]
+        kpos = torch.arange(kh.shape[0])[None, :]
+        return s.masked_fill(kpos > qpos + 1, float("-inf")) if causal else s
     monkeypatch.setattr(A, "_masked_scores", masked)
     _fails(TA.test_first_causal_token)
     _fails(TA.test_zero_query_gives_prefix_mean)
 
 
 def test_missing_numerator_rescale_is_caught(monkeypatch):
-    orig_exp = np.exp
+    import torch
 
     def fold(state, q, kb, vb, qp, kp, causal, scale, qc, kc):
         # fold every tile with the max of its own tile only: correction dropped
@@ -48,14 +50,14 @@ def test_missing_numerator_rescale_is_caught(monkeypatch):
             q1 = min(q.shape[1], q0 + qc)
             for k0 in range(0, kb.shape[1], kc):
                 k1 = min(kb.shape[1], k0 + kc)
-                vis = R._visible(qp + np.arange(q0, q1), kp + np.arange(k0, k1), causal)
-                if not vis.any():
+                vis = R._visible(qp + torch.arange(q0, q1), kp + torch.arange(k0, k1), causal)
+                if not bool(vis.any()):
                     continue
-                s = np.where(vis[None, None], R._scores(q[:, q0:q1], kb[:, k0:k1], scale), -np.inf)
-                m_new = np.maximum(mx[:, :, q0:q1], s.max(axis=3))
-                p = orig_exp(s - m_new[..., None])
-                den[:, :, q0:q1] = den[:, :, q0:q1] + p.sum(axis=3)
-                num[:, q0:q1] = num[:, q0:q1] + np.einsum("bhqk,bkhd->bqhd", p, vb[:, k0:k1])
+                s = R._scores(q[:, q0:q1], kb[:, k0:k1], scale).masked_fill(~vis[None, None], float("-inf"))
+                m_new = torch.maximum(mx[:, :, q0:q1], s.amax(dim=3))
+                p = torch.exp(s - m_new[..., None])
+                den[:, :, q0:q1] = den[:, :, q0:q1] + p.sum(dim=3)
+                num[:, q0:q1] = num[:, q0:q1] + torch.einsum("bhqk,bkhd->bqhd", p, vb[:, k0:k1])
                 mx[:, :, q0:q1] = m_new
     monkeypatch.setattr(R, "_fold_block_fwd", fold)
     _fails(TR.test_ring_forward_equals_naive, 4, True)
