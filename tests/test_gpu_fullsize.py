@@ -117,31 +117,37 @@ def test_host_share_forward_rows_c32768_hosts8(host7):
     c - 1: o and lse against the oracle on those rows (global positions 7c + r)."""
     t = host7
     c, off = t["c"], t["host"] * t["c"]
-    worst = [0.0, 0.0]
+    worst = [0.0, 0.0, 0.0]
     for h in range(t["H"]):
         rows = _tile_rows(c, 128, 300 + h, [0, 1, c - 1])
         hs = slice(h, h + 1)
         o_ref, lse_ref = OA.attention_rows(t["q"][:, :, hs], t["k"][:, :, hs], t["v"][:, :, hs], rows, True,
                                            q_offset=off)
-        worst[0] = max(worst[0], max_err(t["o"][:, rows, hs], o_ref))
+        eo = max_err(t["o"][:, rows, hs], o_ref)
+        worst[0] = max(worst[0], eo)
         worst[1] = max(worst[1], max_err(t["lse"][:, hs][:, :, rows], lse_ref))
-    log("   host 7, one row per query tile of every head: o %.3e lse %.3e" % tuple(worst))
-    assert worst[0] <= TOL_O and worst[1] <= TOL_O
+        worst[2] = max(worst[2], eo / np.abs(o_ref).max())
+    log("   host 7, one row per query tile of every head: o %.3e (%.3e of max |o|) lse %.3e"
+        % (worst[0], worst[2], worst[1]))
+    # rows averaging ~245K values are small (|o| ~ 1e-2): the error is bounded relative to
+    # their magnitude as well, at the tolerance of the plain bound
+    assert worst[0] <= TOL_O and worst[1] <= TOL_O and worst[2] <= TOL_O
 
 
 def test_host_share_dq_rows_c32768_hosts8(host7):
     """dq on one sampled query row of each query tile, in every head, plus rows 0, c - 1."""
     t = host7
     c, off = t["c"], t["host"] * t["c"]
-    worst = 0.0
+    worst, rel = 0.0, 0.0
     for h in range(t["H"]):
         rows = _tile_rows(c, 128, 400 + h, [0, 1, c - 1])
         hs = slice(h, h + 1)
         dq_ref = OA.attention_bwd_rows(t["q"][:, :, hs], t["k"][:, :, hs], t["v"][:, :, hs], t["do"][:, :, hs],
                                        rows, True, q_offset=off)
-        worst = max(worst, max_err(t["dq"][:, rows, hs], dq_ref))
-    log("   host 7, one dq row per query tile of every head: %.3e" % worst)
-    assert worst <= TOL_G
+        e = max_err(t["dq"][:, rows, hs], dq_ref)
+        worst, rel = max(worst, e), max(rel, e / np.abs(dq_ref).max())
+    log("   host 7, one dq row per query tile of every head: %.3e (%.3e of max |dq|)" % (worst, rel))
+    assert worst <= TOL_G and rel <= TOL_G
 
 
 def test_host_share_dkdv_key_rows_c32768_hosts8(host7):
@@ -164,9 +170,11 @@ def test_host_share_dkdv_key_rows_c32768_hosts8(host7):
         dk_ref, dv_ref = dk_ref + dk_s, dv_ref + dv_s
         log("     query rows %d..%d done" % (r0, r0 + 4095))
     ek, ev = max_err(t["dk0"][:, rows], dk_ref), max_err(t["dv0"][:, rows], dv_ref)
-    log("   host 7, %d key rows of head 0: dk %.3e dv %.3e (max |ref| %.3e / %.3e)"
-        % (len(rows), ek, ev, np.abs(dk_ref).max(), np.abs(dv_ref).max()))
-    assert ek <= TOL_G and ev <= TOL_G
+    rk, rv = ek / np.abs(dk_ref).max(), ev / np.abs(dv_ref).max()
+    log("   host 7, %d key rows of head 0: dk %.3e dv %.3e (%.3e / %.3e of max |ref|)" % (len(rows), ek, ev, rk, rv))
+    # one host's contributions are small (|dK|, |dV| ~ 1e-2 here): bounded relative to their
+    # magnitude as well, at the tolerance of the plain gradient bound
+    assert ek <= TOL_G and ev <= TOL_G and rk <= TOL_G and rv <= TOL_G
 
 
 def test_host_share_gradient_sums_c32768_hosts8(host7):
