@@ -190,6 +190,24 @@ int ring_attn_decode(const void* q, const void* k_cache, const void* v_cache, vo
                      hipStream_t stream);
 
 /*
+ * ring_attn_decode for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  Same arguments, same
+ * kernels and the same result as ring_attn_decode, bit for bit, but no allocation of any
+ * kind: the chunk partial states live in a fixed 32 MiB device array (8388608 floats) that
+ * the library holds on every device it runs on until the process ends.  The call needs
+ * B * H * nch * Tq * (D + 2) floats of it, with nch = S / kch chunks, kch = the block
+ * S / n_hosts halved while B * H * nch < 4096 and the half stays a multiple of 32 (e.g.
+ * B = 1, H = 32, D = 128, S = 262144 over 8 hosts: nch = 128, Tq <= 15); larger shapes
+ * return RA_EUNSUPPORTED before anything is enqueued.  Every call on a device uses that
+ * device's one array (nothing in it has to start at zero: each call writes every entry it
+ * reads), so calls that overlap on one device -- on different streams, or from different
+ * threads without ordering -- race and give wrong results; order them on one stream.
+ */
+int ring_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cache, void* o,
+                             float* lse, int B, int H, int S, int D, int Tq, int n_hosts,
+                             int causal, hipStream_t stream);
+
+/*
  * Blockwise feed-forward network (Section 2 equation and "Blockwise Parallel
  * Transformers"; Algorithm 1's feed-forward step), bf16:
  *   y = act(x W1 + b1) W2 + b2, computed `block` rows at a time, so the [rows, d_ff]

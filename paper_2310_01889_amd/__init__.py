@@ -19,6 +19,7 @@ __all__ = [
     "RingAttnError", "library_path", "load", "exported_symbols",
     "ring_attn_fwd", "ring_attn_bwd", "ring_attn_fwd_f32", "ring_attn_bwd_f32",
     "ring_attn_fwd_host", "ring_attn_bwd_host", "ring_attn_fwd_ordered", "ring_attn_decode",
+    "ring_attn_decode_noalloc",
     "blockwise_ffn", "blockwise_ffn_bwd",
     "blockwise_linear", "blockwise_linear_bwd", "ring_layer_fwd", "ring_layer_bwd",
     "rms_norm_fwd", "rms_norm_bwd", "rope_apply", "swiglu_ffn", "swiglu_ffn_bwd",
@@ -46,6 +47,7 @@ _SIGS = {
     "ring_attn_bwd_host": [_P] * 9 + [_I] * 7 + [_P],
     "ring_attn_fwd_ordered": [_P] * 5 + [_I] * 6 + [_P, _P],
     "ring_attn_decode": [_P] * 5 + [_I] * 7 + [_P],
+    "ring_attn_decode_noalloc": [_P] * 5 + [_I] * 7 + [_P],
     "blockwise_ffn": [_P] * 6 + [_I] * 5 + [_P],
     "blockwise_ffn_bwd": [_P] * 10 + [_I] * 5 + [_P],
     "blockwise_linear": [_P] * 4 + [_I] * 4 + [_P],
@@ -255,6 +257,15 @@ def ring_attn_decode(q, k_cache, v_cache, o, lse, n_hosts, causal=True, stream=N
     S = int(k_cache.shape[1])
     bf = torch.bfloat16
     _call("ring_attn_decode", _ptr(q, bf, "q"), _ptr(k_cache, bf, "k_cache"), _ptr(v_cache, bf, "v_cache"),
+          _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"), B, H, S, D, Tq, int(n_hosts), int(causal),
+          _stream(stream))
+
+
+def ring_attn_decode_noalloc(q, k_cache, v_cache, o, lse, n_hosts, causal=True, stream=None):
+    B, Tq, H, D = _bshd(q)
+    S = int(k_cache.shape[1])
+    bf = torch.bfloat16
+    _call("ring_attn_decode_noalloc", _ptr(q, bf, "q"), _ptr(k_cache, bf, "k_cache"), _ptr(v_cache, bf, "v_cache"),
           _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"), B, H, S, D, Tq, int(n_hosts), int(causal),
           _stream(stream))
 

@@ -13,6 +13,8 @@
 // (batch, head, chunk)): the step is a read of the whole cache, bound by HBM bandwidth.
 // A second launch combines the partial states of each (batch, head, query) in ring
 // order, block by block and, inside a block, chunk by chunk, and writes o and lse.
+#include <mutex>
+
 #include "ra_common.h"
 #include "ra_runtime.h"
 #include "ringattn.h"
@@ -304,9 +306,9 @@ int pick_chunk(int B, int H, int S, int c) {
 
 using namespace ra;
 
-extern "C" int ring_attn_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse, int B,
-                                int H, int S, int D, int Tq, int n_hosts, int causal, hipStream_t stream) {
-  g_err.clear();
+// Argument checks shared by both decode entry points.
+static int decode_validate(const void* q, const void* k_cache, const void* v_cache, const void* o, const float* lse,
+                           int B, int H, int S, int D, int Tq, int n_hosts, int causal) {
   if (!q || !k_cache || !v_cache || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
   if (B <= 0 || H <= 0 || S <= 0 || D <= 0 || Tq <= 0 || n_hosts <= 0)
     return set_err(RA_EINVAL, "sizes must be positive (B=%d H=%d S=%d D=%d Tq=%d n_hosts=%d)", B, H, S, D, Tq,
@@ -321,18 +323,21 @@ extern "C" int ring_attn_decode(const void* q, const void* k_cache, const void* 
     return set_err(RA_EUNSUPPORTED, "block S/n_hosts=%d is not a multiple of %d", S / n_hosts, kDecKT);
   if ((long long)B * S * H * D >= (1ll << 31))
     return set_err(RA_EUNSUPPORTED, "B*S*H*D = %lld elements exceeds 2^31-1", (long long)B * S * H * D);
+  return RA_OK;
+}
 
-  const int kch = pick_chunk(B, H, S, S / n_hosts);
+// Both launches of a decode call, the chunk partial states in `part` (rows * (D + 2) floats
+// for rows = B * H * nch * Tq, every entry written by the first launch before the second
+// reads it).
+static int decode_launch(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse, int B, int H,
+                         int S, int D, int Tq, int n_hosts, int causal, int kch, float* part, hipStream_t stream) {
   const int nch = S / kch;
   const long long rows = (long long)B * H * nch * Tq;
-  CallResources R(stream);
-  int rc = R.alloc((size_t)rows * (D + 2) * sizeof(float));
-  if (rc) return rc;
   DecodeArgs da;
   da.q = (const bf16*)q;
   da.k = (const bf16*)k_cache;
   da.v = (const bf16*)v_cache;
-  da.part_acc = (float*)R.ws;
+  da.part_acc = part;
   da.part_m = da.part_acc + rows * D;
   da.part_l = da.part_m + rows;
   da.B = B;
@@ -358,4 +363,64 @@ extern "C" int ring_attn_decode(const void* q, const void* k_cache, const void* 
     hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(B * H * Tq), dim3(64 * kMergeWaves), 0, stream, ma);
   RA_HIP(hipGetLastError());
   return RA_OK;
+}
+
+extern "C" int ring_attn_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse, int B,
+                                int H, int S, int D, int Tq, int n_hosts, int causal, hipStream_t stream) {
+  g_err.clear();
+  int rc = decode_validate(q, k_cache, v_cache, o, lse, B, H, S, D, Tq, n_hosts, causal);
+  if (rc) return rc;
+  const int kch = pick_chunk(B, H, S, S / n_hosts);
+  const long long rows = (long long)B * H * (S / kch) * Tq;
+  CallResources R(stream);
+  if ((rc = R.alloc((size_t)rows * (D + 2) * sizeof(float)))) return rc;
+  return decode_launch(q, k_cache, v_cache, o, lse, B, H, S, D, Tq, n_hosts, causal, kch, (float*)R.ws, stream);
+}
+
+// ---------------------------------------------------------------------------------
+// Decode without allocation.  The chunk partial states live in a fixed device array of
+// kScratchFloats floats that every device the library runs on holds until the process
+// ends.  In host code `scratch` names a host-side stand-in, not device memory: the device
+// address of each device's copy is looked up once per device, with that device current,
+// and only that address is handed to the kernels.
+// ---------------------------------------------------------------------------------
+constexpr long long kScratchFloats = 8ll << 20;  // 32 MiB
+static __device__ __align__(256) float scratch[kScratchFloats];
+
+namespace {
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[64];
+
+int scratch_ptr(float** out) {
+  int dev = 0;
+  RA_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return set_err(RA_EHIP, "device index %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    RA_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return set_err(RA_EHIP, "hipGetSymbolAddress returned a null address for the decode scratch");
+    g_scratch_ptr[dev] = (float*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return RA_OK;
+}
+}  // namespace
+
+extern "C" int ring_attn_decode_noalloc(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
+                                        int B, int H, int S, int D, int Tq, int n_hosts, int causal,
+                                        hipStream_t stream) {
+  g_err.clear();
+  int rc = decode_validate(q, k_cache, v_cache, o, lse, B, H, S, D, Tq, n_hosts, causal);
+  if (rc) return rc;
+  const int kch = pick_chunk(B, H, S, S / n_hosts);
+  const long long need = (long long)B * H * (S / kch) * Tq * (D + 2);
+  if (need > kScratchFloats)
+    return set_err(RA_EUNSUPPORTED,
+                   "partial state of %lld floats (B*H*(S/%d)*Tq*(D+2)) exceeds the %lld-float scratch of "
+                   "ring_attn_decode_noalloc",
+                   need, kch, kScratchFloats);
+  float* part = nullptr;
+  if ((rc = scratch_ptr(&part))) return rc;
+  return decode_launch(q, k_cache, v_cache, o, lse, B, H, S, D, Tq, n_hosts, causal, kch, part, stream);
 }
