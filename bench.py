@@ -16,11 +16,13 @@ launch, on the stream it runs on) against the bf16 dense matrix-core peak, and b
 against the rate the chip sustains on back-to-back matrix products alone (the library's
 calibration kernel, measured in the same run).  `ms_per_step` is the mean over the timed
 calls, with their median and minimum alongside.  The
-`cpu_baseline` object times the fp64 CPU oracle on one head of the same workload and
-scales it to all 32 heads.  `extra` holds secondary configurations measured in the same
-run (forward+backward at S=16384, one host's share at 262144 tokens, ring decode of 1 and 8
-tokens against a 262144-token cache, blockwise FFN, the Algorithm 1 layer and a 2-layer
-LLaMA-style training step) for context.
+`cpu_baseline` object times the blockwise fp64 ring oracle (torch CPU) on one head of the
+same workload and scales it to all 32 heads.  `extra` holds secondary configurations
+measured in the same run (forward+backward at S=16384, one host's share at 262144 tokens,
+forward and forward+backward, ring decode of 1 and 8 tokens against a 262144-token cache,
+blockwise FFN, the Algorithm 1 layer and a 2-layer LLaMA-style training step) for context,
+and the same CPU oracle timed on bounded samples of the S=16384 forward+backward and of the
+host share.
 """
 import argparse
 import json
@@ -107,28 +109,65 @@ def cpu_model():
     return "unknown"
 
 
-def cpu_baseline(B, S, H, D):
-    """fp64 oracle on one head of the workload, scaled to all heads."""
+def _torch_threads():
+    import torch
+    return int(torch.get_num_threads())
+
+
+def cpu_baseline(B, S, H, D, N):
+    """The blockwise ring oracle (fp64, torch CPU) on one head of the workload, scaled to
+    all heads."""
     import numpy as np
-    from threadpoolctl import threadpool_info
-    from oracle import attention as OA
+    from oracle import ring as OR
     rng = np.random.default_rng(0)
     q, k, v = (rng.standard_normal((B, S, 1, D)) for _ in range(3))
     t0 = time.perf_counter()
-    OA.attention_fwd(q, k, v, True)
+    OR.ring_attention_fwd(q, k, v, N, True)
     dt = time.perf_counter() - t0
     flops_one_head = 4.0 * B * D * causal_pairs(S)
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {
         "value": flops_one_head / dt / 1e12,
         "unit": "TFLOP/s",
-        "cores": int(threads),
+        "cores": _torch_threads(),
         "cpu_model": cpu_model(),
         "kind": "oracle",
-        "sample": "oracle.attention.attention_fwd (fp64, NumPy BLAS) on 1 of %d heads of the "
-                  "workload (B=%d, S=%d, D=%d, causal): %.1f s; whole workload extrapolated "
-                  "linearly to %.0f s" % (H, B, S, D, dt, dt * H),
+        "sample": "oracle.ring.ring_attention_fwd (blockwise ring oracle, fp64, torch CPU; %d hosts, tiles of "
+                  "one block) on 1 of %d heads of the workload (B=%d, S=%d, D=%d, causal): %.1f s; whole "
+                  "workload extrapolated linearly to %.0f s" % (N, H, B, S, D, dt, dt * H),
     }
+
+
+def cpu_baselines_other():
+    """The blockwise ring oracle timed on bounded samples of the other attention
+    configurations: forward + backward at S=16384 (1 of 16 heads), and one host's share
+    (host 7 of 8, c=32768; 1 of 32 heads, its first 2 of 8 ring steps, tiles of 4096),
+    each extrapolated linearly to the whole configuration."""
+    import numpy as np
+    from oracle import ring as OR
+    rng = np.random.default_rng(1)
+    out = {}
+    S3, H3, N3, D = 16384, 16, 8, 128
+    q, k, v, do = (rng.standard_normal((1, S3, 1, D)) for _ in range(4))
+    t0 = time.perf_counter()
+    OR.ring_attention_bwd(q, k, v, do, N3, True)  # recomputes the forward: forward + backward
+    dt = time.perf_counter() - t0
+    f = 4.0 * D * causal_pairs(S3) * 3.5
+    out["fwd_bwd_S16384_H16"] = {"tflops": round(f / dt / 1e12, 5), "sample_s": round(dt, 2),
+                                 "whole_s_extrapolated": round(dt * H3, 1), "cores": _torch_threads(),
+                                 "sample": "1 of 16 heads, ring forward + backward"}
+    c5, N5, H5 = 32768, 8, 32
+    qb = rng.standard_normal((1, c5, 1, D))
+    kk, vv = rng.standard_normal((1, N5 * c5, 1, D)), rng.standard_normal((1, N5 * c5, 1, D))
+    t0 = time.perf_counter()
+    OR.ring_host_fwd(qb, kk, vv, N5, 7, True, query_chunk=4096, key_chunk=4096, blocks=2)
+    dt = time.perf_counter() - t0
+    done = c5 * (c5 + 1) / 2 + c5 * c5  # the diagonal block and one full block
+    whole = host_pairs(c5, 7, N5) * H5
+    out["host7_of_8_c32768_H32"] = {"tflops": round(4.0 * D * done / dt / 1e12, 5), "sample_s": round(dt, 2),
+                                    "whole_s_extrapolated": round(dt * whole / done, 1),
+                                    "cores": _torch_threads(),
+                                    "sample": "1 of 32 heads, the first 2 of 8 ring steps (diagonal + one full block)"}
+    return out
 
 
 def recorded_traffic():
@@ -181,7 +220,31 @@ def run_extras(ra, torch, mk, g, D, steps, only):
         f5 = 4.0 * H5 * D * host_pairs(c5, 7, N5)
         extra["host7_of_8_c32768_H32"] = {"ms": round(ms5, 3), "tflops": round(f5 / ms5 / 1e9, 2),
                                           "query_tokens_per_s": round(c5 / (ms5 * 1e-3), 1)}
-        del qb, ob, lb
+        # the same share forward + backward: dq local, the float32 dK/dV every block carries
+        # received with it through the double buffer, added to and passed on
+        dob, dqb = mk(1, c5, H5, D), torch.empty_like(qb)
+        dka = torch.zeros((1, N5 * c5, H5, D), dtype=torch.float32, device="cuda")
+        dva = torch.zeros_like(dka)
+
+        def fb5():
+            ra.ring_attn_fwd_host(qb, k5, v5, ob, lb, N5, 7, True)
+            ra.ring_attn_bwd_host(qb, k5, v5, ob, lb, dob, dqb, dka, dva, N5, 7, True)
+        for _ in range(2):
+            fb5()
+        torch.cuda.synchronize()
+        ra.timing_read(ra.KERNEL_ATTN_BWD)
+        ra.timing_enable(True)
+        msb, _ = time_calls(fb5, 3, 0)
+        ra.timing_enable(False)
+        kb, nb = ra.timing_read(ra.KERNEL_ATTN_BWD)
+        ra.timing_read(ra.KERNEL_ATTN_FWD)
+        extra["host7_of_8_c32768_H32_fwd_bwd"] = {
+            "ms": round(msb, 3), "tflops": round(3.5 * f5 / msb / 1e9, 2),
+            "query_tokens_per_s": round(c5 / (msb * 1e-3), 1),
+            "bwd_step_kernels_ms": round(kb / 3, 3), "bwd_launches_per_call": nb // 3,
+            "bwd_tflops": round(2.5 * f5 / (kb / 3) / 1e9, 2),
+            "note": "algorithmic flops: forward + 2.5x for the backward (5 contractions incl. the recompute)"}
+        del qb, ob, lb, dob, dqb, dka, dva
     if want("decode"):
         # ring decode against the same 262144-token cache (8 hosts x 32768), 1 and 8 new tokens
         for tq in (1, 8):
@@ -337,7 +400,9 @@ def main():
     if not args.no_extra:
         out["extra"] = run_extras(ra, torch, mk, g, D, args.steps, None)
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(B, S, H, D)
+        out["cpu_baseline"] = cpu_baseline(B, S, H, D, N)
+        if not args.no_extra:
+            out.setdefault("extra", {})["cpu_oracle_other_configs"] = cpu_baselines_other()
     print(json.dumps(out), flush=True)
 
 
