@@ -389,33 +389,56 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
 
   // add into the float32 gradient of the block (its home rows); dK carries the 1/sqrt(D).
   // The block's first contribution is written, not added; its last goes out in bf16.
+  // Every carried value is loaded before the first store (the compiler cannot tell the dV
+  // loads from the dK stores, and would otherwise wait for one memory round trip per
+  // 16-byte piece).
   const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key_in_blk) * rs + h * D;
   const int kf = p.dkv_flags[slot];
+  f32x4 kin[NDT][4], vin[NDT][4];
+  if (kf & kFirst) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) kin[dt][gg] = vin[dt][gg] = f32x4{0.f, 0.f, 0.f, 0.f};
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int d = 32 * dt + 8 * gg + 4 * hi;
+        kin[dt][gg] = *(const f32x4*)(p.dk + grow + d);
+        vin[dt][gg] = *(const f32x4*)(p.dv + grow + d);
+      }
+  }
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-    for (int gg = 0; gg < 4; ++gg) {
-      const int d = 32 * dt + 8 * gg + 4 * hi;
-      f32x4* dkp = (f32x4*)(p.dk + grow + d);
-      f32x4* dvp = (f32x4*)(p.dv + grow + d);
-      f32x4 k4 = {0.f, 0.f, 0.f, 0.f}, v4 = {0.f, 0.f, 0.f, 0.f};
-      if (!(kf & kFirst)) {
-        k4 = *dkp;
-        v4 = *dvp;
-      }
+    for (int gg = 0; gg < 4; ++gg)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        k4[e] += dkacc[dt][4 * gg + e] * p.scale;
-        v4[e] += dvacc[dt][4 * gg + e];
+        kin[dt][gg][e] += dkacc[dt][4 * gg + e] * p.scale;
+        vin[dt][gg][e] += dvacc[dt][4 * gg + e];
       }
-      if (kf & kLast) {
+  if (kf & kLast) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int d = 32 * dt + 8 * gg + 4 * hi;
+        const f32x4 k4 = kin[dt][gg], v4 = vin[dt][gg];
         *(u32x2*)((bf16*)p.dk_out + grow + d) = u32x2{pack_bf16x2(k4[0], k4[1]), pack_bf16x2(k4[2], k4[3])};
         *(u32x2*)((bf16*)p.dv_out + grow + d) = u32x2{pack_bf16x2(v4[0], v4[1]), pack_bf16x2(v4[2], v4[3])};
-      } else {
-        *dkp = k4;
-        *dvp = v4;
       }
-    }
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int d = 32 * dt + 8 * gg + 4 * hi;
+        *(f32x4*)(p.dk + grow + d) = kin[dt][gg];
+        *(f32x4*)(p.dv + grow + d) = vin[dt][gg];
+      }
+  }
 }
 
 // =====================================================================================
@@ -601,20 +624,31 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   float* dqrow = p.dq + qoff;
   const bool first = p.dq_out != nullptr && (hs.flags & kFirst);
   const bool fin = p.dq_out != nullptr && (hs.flags & kLast);
+  // all carried values loaded before the first store (one memory round trip, not 16)
+  f32x4 qin[NDT][4];
+  if (first) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) qin[dt][gg] = f32x4{0.f, 0.f, 0.f, 0.f};
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) qin[dt][gg] = *(const f32x4*)(dqrow + 32 * dt + 8 * gg + 4 * hi);
+  }
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
     for (int gg = 0; gg < 4; ++gg) {
       const int d = 32 * dt + 8 * gg + 4 * hi;
-      f32x4* dp = (f32x4*)(dqrow + d);
-      f32x4 t = {0.f, 0.f, 0.f, 0.f};
-      if (!first) t = *dp;
+      f32x4 t = qin[dt][gg];
 #pragma unroll
       for (int e = 0; e < 4; ++e) t[e] += dqacc[dt][4 * gg + e] * p.scale;
       if (fin)
         *(u32x2*)((bf16*)p.dq_out + qoff + d) = u32x2{pack_bf16x2(t[0], t[1]), pack_bf16x2(t[2], t[3])};
       else
-        *dp = t;
+        *(f32x4*)(dqrow + d) = t;
     }
 }
 
