@@ -31,8 +31,7 @@ namespace ra {
 namespace {
 
 constexpr int kBM = 128, kBN = 64, kThreads = 256;
-constexpr float kTau = 8.f;  // lazy-rescale threshold (log2 units)
-constexpr int kPF = 2;       // LDS operand reads issued this many schedule steps ahead
+constexpr float kSumMax = 65536.f;  // overflow test: a lane's row sum over a tile below this
 
 
 // LDS tiles are unpadded [64 rows][D] with the 16-byte chunks of each row permuted by
@@ -129,42 +128,41 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   // ---- Q in registers: B operand of S^T = K Q^T (n = query, k = dim) ---------------
   // Q as stored (bf16): the products q.k are exact in the float32 accumulators, and the
   // scale log2(e)/sqrt(D) is applied in float32 (the paper's float32 logits), once per
-  // score, right before its exponential.
+  // score, fused with the subtraction of the running maximum: x = fma(q.k, sl2, -m_eff).
   const float sl2 = p.scale * kLog2e;
-  const float isl2 = 1.f / sl2;
   bf16x8 qreg[NKK];
   {
     const bf16* qrow = qbase + (long long)qr * rs;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) qreg[kk] = *(const bf16x8*)(qrow + 16 * kk + 8 * hi);
   }
-  // Scores in log2 units are sl2 * q.k.  The score accumulators start from -m_eff / sl2
-  // (m_eff = running maximum in log2 units, 0 while it is still -inf), so each MFMA chain
-  // yields (s - m_eff) / sl2, and one multiply as soon as a tile's chains are complete
-  // gives s - m_eff, the exponent.  thr: a row whose new scores exceed it forces a
-  // rescale (kTau above the maximum, any visible key at all while the maximum is still
-  // -inf).
+  // Running maximum without a per-tile maximum.  m_eff = the running maximum in log2 units
+  // (0 while it is still -inf); the probabilities of a tile are formed against it, and the
+  // tile's exact maximum is taken -- m raised, O^T and l rescaled, the probabilities formed
+  // again -- only when a lane's row sum over the tile is not below kSumMax (or not finite),
+  // or while m is still -inf (thrs = -1).  Every probability that reaches the products is
+  // thus at most kSumMax, which bf16 and float32 hold exactly in range; the offset cancels
+  // in o and is carried in lse.
   float m_eff = (m_run == -INFINITY) ? 0.f : m_run;
-  float thr = (m_run == -INFINITY) ? -INFINITY : kTau;
-  f32x16 minit;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) minit[i] = -m_eff * isl2;
+  float thrs = (m_run == -INFINITY) ? -1.f : kSumMax;
+  const f32x16 zero16 = {};
 
-  // ---- direct-to-LDS staging: each wave fills 16 rows of a tile ---------------------
-  // load j of a wave covers rows wave*RPW + j*ROWS_PER_LOAD + lane / CPR; the lane's
-  // physical chunk is lane % CPR, its logical (global) chunk that ^ swz(row).
-  int goff[LOADS];  // byte offsets from the tile base
-#pragma unroll
-  for (int j = 0; j < LOADS; ++j) {
-    const int r = wave * RPW + j * ROWS_PER_LOAD + lane / CPR;
-    goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
-  }
+  // ---- direct-to-LDS staging: each wave fills RPW rows of a tile ---------------------
+  // load j of wave w covers rows j * 4 ROWS_PER_LOAD + w ROWS_PER_LOAD + lane / CPR; the
+  // lane's physical chunk is lane % CPR, its logical (global) chunk that ^ swz(row).  With
+  // rows interleaved over the waves this way, swz(row) is the same for all loads of a lane
+  // (the row bits it reads do not depend on j), so every load of the lane reads at one
+  // byte offset goff plus a wave-uniform j * 8 ROWS_PER_LOAD * rs bytes.
+  static_assert(RPW == LOADS * ROWS_PER_LOAD, "each wave fills LOADS row groups");
+  const int goff = 2 * ((wave * ROWS_PER_LOAD + lane / CPR) * rs +
+                        8 * ((lane % CPR) ^ swz<D>(wave * ROWS_PER_LOAD + lane / CPR)));
   // buffer loads with the LDS flag: the tile base is a wave-uniform descriptor, so the
   // per-tile address update is scalar work; reads past the tile return zero
   auto dload = [&](const bf16* src_tile, bf16* dst_tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j)
-      buffer_load_lds16(src_tile, kBN * rs * 2, dst_tile + (wave_u * RPW + j * ROWS_PER_LOAD) * D, goff[j]);
+      buffer_load_lds16_so(src_tile, kBN * rs * 2, dst_tile + (j * 4 + wave_u) * ROWS_PER_LOAD * D, goff,
+                           j * 8 * ROWS_PER_LOAD * rs);
   };
   auto load_k = [&](int it, auto Bc) __attribute__((always_inline)) { dload(kbase + (long long)it * kBN * rs, kbuf(Bc)); };
   auto load_v = [&](int it, auto Bc) __attribute__((always_inline)) { dload(vbase + (long long)it * kBN * rs, vbuf(Bc)); };
@@ -187,74 +185,25 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
       voff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
     }
 
-  // S^T = K Q^T for the 64 keys of K buffer `buf` x this wave's 32 queries
-  auto scores = [&](const bf16* kt, f32x16* sacc) __attribute__((always_inline)) {
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      sacc[mt] = mfma32(*(const bf16x8*)(kt + 32 * mt * D + koff[0]), qreg[0], minit);
-#pragma unroll
-      for (int kk = 1; kk < NKK; ++kk)
-        sacc[mt] = mfma32(*(const bf16x8*)(kt + 32 * mt * D + koff[kk]), qreg[kk], sacc[mt]);
-    }
-  };
+  // ---- three-stage tile pipeline -----------------------------------------------------
+  // Region t (one straight-line stretch of code per tile): the score products of tile t+1
+  // (into s_nx), the exponentials of tile t (from s_cur, into the packed probabilities w)
+  // and O^T += V^T P^T of tile t-1 (from pprev), interleaved step by step; the overflow
+  // test of tile t closes the region, so that the only branch (the rare exact path) sits
+  // between regions and tile t's probabilities are known good before tile t+1's region
+  // multiplies them into O^T.  K runs one tile ahead of the scores, V one tile behind.
+  // Region t reads K(t+1) and V(t-1) from buffer (t+1) % 2 and loads K(t+2), V(t) into
+  // buffer t % 2.
+  constexpr int NS = 2 * NKK;    // score products per tile (two 32-key halves)
+  constexpr int NP = 4 * NDT;    // PV products per tile (four 16-key groups)
+  constexpr int NSTEP = NS + NP;
+  constexpr int PF = 2;          // operand reads issued this many steps ahead
+  static_assert(NS == NP, "as many score as PV products per tile");
+  f32x16 s_cur[2], s_nx[2];      // raw q.k of tiles t and t+1 (masked keys -inf)
+  bf16x8 pprev[4];               // P^T of tile t-1, four 16-key groups
+  float l_tile = 0.f;            // this lane's row sum of tile t's probabilities
 
-  // ---- pipeline: K runs one tile ahead of V ------------------------------------------
-  // While tile it is processed, LDS holds K tiles it, it+1 and V tile it; loads of K tile
-  // it+2 (into the buffer of K tile it) and V tile it+1 (into the buffer of V tile it-1)
-  // are in flight.  One straight-line region per tile issues the scores of tile it+1 on
-  // the matrix cores, the exponentials of tile it on the vector ALUs and O += V P for
-  // tile it, interleaved (sched_group_barrier); the running-max decision for tile it+1
-  // closes the region, so the only branch (the rare rescale) sits between tiles.
-  // Lazy rescale (online softmax, log2 domain).  Each lane owns one query; the partner
-  // lane l^32 holds the other half of its keys.  The running maximum is raised only
-  // when a row's new scores exceed it by more than kTau, so probabilities stay below
-  // 2^kTau and the rescale of the accumulator -- a wave-uniform branch -- is rare.
-  // mx: this lane's maximum of the tile's s - m_eff; sc: the tile's scores (s - m_eff,
-  // log2 units), shifted here to the new maximum.
-  auto rescale = [&](float mx, f32x16* sc) __attribute__((always_inline)) {
-    const float mx2 = pair_max(mx);
-    if (__builtin_amdgcn_ballot_w64(mx2 > thr)) {
-      const float m_new = fmaxf(m_run, m_eff + mx2);
-      const float m_new_eff = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
-      const float delta = m_new_eff - m_eff;
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sc[mt][i] -= delta;
-      m_run = m_new;
-      m_eff = m_new_eff;
-      thr = (m_new == -INFINITY) ? -INFINITY : kTau;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) minit[i] = -m_eff * isl2;
-    }
-  };
-  auto scale_half = [&](f32x16* sc, int mt) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) sc[mt][i] *= sl2;
-  };
-  auto decide = [&](f32x16* sc) __attribute__((always_inline)) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[mt][i]);
-    rescale(mx, sc);
-  };
-  auto mask_half = [&](f32x16* sc, int mt, int it) __attribute__((always_inline)) {
-    const int kpos0 = hs.k_pos0 + it * kBN;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
-      if (kpos > qpos) sc[mt][i] = -INFINITY;
-    }
-  };
-  auto mask = [&](f32x16* sc, int it) __attribute__((always_inline)) {
+  auto mask_tile = [&](f32x16* sc, int it) __attribute__((always_inline)) {
     const int kpos0 = hs.k_pos0 + it * kBN;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
@@ -264,206 +213,224 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
         if (kpos > qpos) sc[mt][i] = -INFINITY;
       }
   };
-  // P = exp2(s log2e/sqrt(D) - m) in bf16 and O^T += V^T P^T for one tile
-  auto softmax_pv = [&](const f32x16* sc, const bf16* vt) __attribute__((always_inline)) {
-    float rsum = 0.f;
+  // probabilities of pair u (keys 2u, 2u+1 of this lane's 32) of a tile, packed bf16
+  auto expo_pair = [&](const f32x16* sc, int u) __attribute__((always_inline)) -> uint32_t {
+    const int kb = u / 4, jj = u % 4, i0 = 8 * (kb & 1) + 2 * jj;
+    return pack_bf16x2(fast_exp2(fmaf(sc[kb >> 1][i0], sl2, -m_eff)), fast_exp2(fmaf(sc[kb >> 1][i0 + 1], sl2, -m_eff)));
+  };
+  // exact path of a tile whose probabilities failed the test: its maximum, the rescale of
+  // the state, the probabilities again (w, l_tile)
+  auto exact = [&](const f32x16* sc, uint32_t* w) __attribute__((always_inline)) {
+    float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      u32x4 w;
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float p0 = fast_exp2(sc[kb >> 1][8 * (kb & 1) + 2 * j]);
-        const float p1 = fast_exp2(sc[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
-        w[j] = pack_bf16x2(p0, p1);
-        rsum = dot2_bf16_ones(w[j], rsum);  // row sum of the bf16 probabilities used
-      }
-      const bf16x8 pb = __builtin_bit_cast(bf16x8, w);
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[mt][i]);
+    const float mx2 = pair_max(mx) * sl2;  // masked keys -inf; every scale positive
+    const float m_new = fmaxf(m_run, mx2);
+    const float alpha = (m_run == -INFINITY) ? 0.f : fast_exp2(m_run - m_new);
+    l_run *= alpha;
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x4 lo = lds_read_tr16(vt + 16 * kb * D + voff[0][dt]);
-        const bf16x4 up = lds_read_tr16(vt + 16 * kb * D + voff[1][dt]);
-        const bf16x8 a = {lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-        oacc[dt] = mfma32(a, pb, oacc[dt]);
-      }
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) oacc[dt][i] *= alpha;
+    m_run = m_new;
+    m_eff = (m_new == -INFINITY) ? 0.f : m_new;
+    thrs = (m_new == -INFINITY) ? -1.f : kSumMax;
+    float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      w[u] = expo_pair(sc, u);
+      if (u & 1) r1 = dot2_bf16_ones(w[u], r1); else r0 = dot2_bf16_ones(w[u], r0);
     }
-    l_run += rsum;
+    l_tile = r0 + r1;
+  };
+  // end of region: the test, then the tile's probabilities become pprev
+  auto close_tile = [&](const f32x16* sc, uint32_t* w) __attribute__((always_inline)) {
+    if (__builtin_amdgcn_ballot_w64(!(l_tile < thrs))) exact(sc, w);
+    l_run += l_tile;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) pprev[kb] = __builtin_bit_cast(bf16x8, u32x4{w[4 * kb], w[4 * kb + 1], w[4 * kb + 2], w[4 * kb + 3]});
   };
 
-  if (nt > 0) {
-    load_k(0, I0{});
-    load_v(0, I0{});
-    if (nt > 1) load_k(1, I1{});
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  f32x16 s_cur[2];
-  if (nt > 0) {
-    scores(sK0, s_cur);
-    scale_half(s_cur, 0);
-    scale_half(s_cur, 1);
-    if (n_full == 0) mask(s_cur, 0);
-    decide(s_cur);
-  }
-  // the first loop step reloads the buffer of K tile 0: every wave must have read it
-  if (nt > 2) __syncthreads();
-
-  // tile it with a successor; B = it & 1 at compile time, MN: tile it+1 needs the mask.
-  // The region is laid out by hand in 20 steps separated by scheduling fences: step s
-  // issues the LDS reads of the operands kPF steps ahead, the score MFMA s of tile it+1
-  // (s < 16), the O += V P MFMA s-4 of tile it (s >= 4), and a quarter of the exponentials
-  // of one 16-key group of tile it (s < 16; group g is consumed from step 4g + 4 on) or
-  // part of the next row maximum (s >= 16).
-  auto body_sched = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+  // Region t.  Bc = t % 2 (buffer loaded), NX: tile t+1 exists, PV: tile t-1 exists, MC:
+  // tile t needs the causal mask.  Step s issues MFMA s -- the PV products of tile t-1 in
+  // the first half of the region, the score products of tile t+1 in the second, so that
+  // the probabilities of tile t-1 and the scores of tile t+1 are never live together --,
+  // operand reads PF steps ahead, and the vector work of pair u = s * 16 / NSTEP of tile t:
+  // its exponentials at that step, its packing one step later, its row-sum term two steps
+  // later.
+  auto region = [&](auto Bc, auto NXc, auto PVc, auto MCc, int it, bool RTMASK = false) __attribute__((always_inline)) {
     constexpr int B = decltype(Bc)::value;
-    constexpr bool MN = decltype(Mc)::value;
-    static_assert(NKK == 8 && NDT == 4, "hand schedule written for D = 128");
-    if (it + 2 < nt) load_k(it + 2, Bc);
-    load_v(it + 1, std::integral_constant<int, B ^ 1>{});
+    constexpr bool NX = decltype(NXc)::value, PV = decltype(PVc)::value, MC = decltype(MCc)::value;
+    if (NX && it + 2 < nt) load_k(it + 2, Bc);
+    load_v(it, Bc);  // read by region t+1 or, after the last region, by the final products
     const bf16* kt = kbuf(std::integral_constant<int, B ^ 1>{});
-    const bf16* vt = vbuf(Bc);
-    f32x16 s_next[2];
-    bf16x8 kop[16], vop[16], pb[4];
-    uint32_t w[4][4];
+    const bf16* vt = vbuf(std::integral_constant<int, B ^ 1>{});
+    if constexpr (MC) mask_tile(s_cur, it);
+    if constexpr (!MC) {
+      if (RTMASK && it >= n_full) mask_tile(s_cur, it);
+    }
+    bf16x8 kop[NS], vop[NP];
+    uint32_t w[16];
+    float pe[16][2];
     float rs2[4] = {0.f, 0.f, 0.f, 0.f};
-    float mxa = -INFINITY, mxb = -INFINITY;
-    // score MFMA S: the two 32-key halves alternate (mt = S % 2, kk = S / 2), so that
-    // consecutive score MFMAs are independent
-    auto read_k = [&](auto Sc) __attribute__((always_inline)) {
+    auto fetch = [&](auto Sc) __attribute__((always_inline)) {
       constexpr int S = decltype(Sc)::value;
-      kop[S] = *(const bf16x8*)(kt + 32 * (S % 2) * D + koff[S / 2]);
-    };
-    auto read_v = [&](auto Sc) __attribute__((always_inline)) {
-      constexpr int S = decltype(Sc)::value;  // PV MFMA S: kb = S / NDT, dt = S % NDT
-      const bf16x4 lo = lds_read_tr16(vt + 16 * (S / NDT) * D + voff[0][S % NDT]);
-      const bf16x4 up = lds_read_tr16(vt + 16 * (S / NDT) * D + voff[1][S % NDT]);
-      vop[S] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
-    };
-    // 21 steps.  Step S: score MFMA S (S < 16); PV MFMA S - 5 (S >= 5); the exponentials of
-    // pair S (S < 16), the bf16 packing of pair S - 1 and the row-sum update of pair S - 2,
-    // so that no step waits on a result of its own; the next tile's masking and maximum
-    // from step 16 on (the last score MFMAs issue at steps 14 and 15).
-    float pe0[16], pe1[16];
-    constexpr int kPVD = 5;
-    static_for<0, kPF>([&](auto Sc) __attribute__((always_inline)) { read_k(Sc); });
-    static_for<0, 16 + kPVD>([&](auto Sc) __attribute__((always_inline)) {
-      constexpr int S = decltype(Sc)::value;
-      if constexpr (S + kPF < 16) read_k(std::integral_constant<int, S + kPF>{});
-      if constexpr (S + kPF >= kPVD && S + kPF < 16 + kPVD) read_v(std::integral_constant<int, S + kPF - kPVD>{});
-      if constexpr (S < 16) {
-        constexpr int mt = S % 2, kk = S / 2;
-        s_next[mt] = mfma32(kop[S], qreg[kk], kk == 0 ? minit : s_next[mt]);
-      }
-      if constexpr (S >= kPVD) {
-        constexpr int q = S - kPVD, kb = q / NDT, dt = q % NDT;
-        if constexpr (dt == 0) pb[kb] = __builtin_bit_cast(bf16x8, u32x4{w[kb][0], w[kb][1], w[kb][2], w[kb][3]});
-        oacc[dt] = mfma32(vop[q], pb[kb], oacc[dt]);
-      }
-      if constexpr (S < 16) {
-        constexpr int kb = S / 4, j = S % 4;
-        pe0[S] = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j]);
-        pe1[S] = fast_exp2(s_cur[kb >> 1][8 * (kb & 1) + 2 * j + 1]);
-      }
-      if constexpr (S >= 1 && S <= 16) {
-        constexpr int P = S - 1;
-        w[P / 4][P % 4] = pack_bf16x2(pe0[P], pe1[P]);
-      }
-      if constexpr (S >= 2 && S <= 17) {
-        constexpr int P = S - 2;
-        rs2[P % 4] = dot2_bf16_ones(w[P / 4][P % 4], rs2[P % 4]);  // row sum of the bf16 probabilities used
-      }
-      if constexpr (S == 16 || S == 17) {
-        if constexpr (S == 16) scale_half(s_next, 0);
-        if constexpr (S == 16 && MN) mask_half(s_next, 0, it + 1);
-#pragma unroll
-        for (int i = 8 * (S - 16); i < 8 * (S - 15); ++i) mxa = fmaxf(mxa, s_next[0][i]);
-      } else if constexpr (S >= 18) {
-        if constexpr (S == 18) scale_half(s_next, 1);
-        if constexpr (S == 18 && MN) mask_half(s_next, 1, it + 1);
-        if constexpr (S < 20) {
-#pragma unroll
-          for (int i = 8 * (S - 18); i < 8 * (S - 17); ++i) mxb = fmaxf(mxb, s_next[1][i]);
+      if constexpr (S >= NP) {
+        constexpr int I = S - NP;  // score product I: key half I % 2, dims 16 (I / 2)..
+        if constexpr (NX) kop[I] = *(const bf16x8*)(kt + 32 * (I % 2) * D + koff[I / 2]);
+      } else {
+        constexpr int Q = S;  // PV product Q: keys 16 (Q / NDT).., dims 32 (Q % NDT)..
+        if constexpr (PV) {
+          const bf16x4 lo = lds_read_tr16(vt + 16 * (Q / NDT) * D + voff[0][Q % NDT]);
+          const bf16x4 up = lds_read_tr16(vt + 16 * (Q / NDT) * D + voff[1][Q % NDT]);
+          vop[Q] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
         }
+      }
+    };
+    constexpr int UPS = NSTEP / 16;  // steps per probability pair
+    static_for<0, PF>([&](auto Sc) __attribute__((always_inline)) { fetch(Sc); });
+    static_for<0, NSTEP + 2 * UPS>([&](auto Sc) __attribute__((always_inline)) {
+      constexpr int S = decltype(Sc)::value;
+      if constexpr (S + PF < NSTEP) fetch(std::integral_constant<int, S + PF>{});
+      if constexpr (S < NSTEP && S >= NP) {
+        constexpr int I = S - NP, mt = I % 2, kk = I / 2;
+        if constexpr (NX) s_nx[mt] = mfma32(kop[I], qreg[kk], kk == 0 ? zero16 : s_nx[mt]);
+      } else if constexpr (S < NP) {
+        constexpr int Q = S;
+        if constexpr (PV) oacc[Q % NDT] = mfma32(vop[Q], pprev[Q / NDT], oacc[Q % NDT]);
+      }
+      if constexpr (S % UPS == 0 && S / UPS < 16) {
+        constexpr int u = S / UPS, kb = u / 4, jj = u % 4, i0 = 8 * (kb & 1) + 2 * jj;
+        pe[u][0] = fast_exp2(fmaf(s_cur[kb >> 1][i0], sl2, -m_eff));
+        pe[u][1] = fast_exp2(fmaf(s_cur[kb >> 1][i0 + 1], sl2, -m_eff));
+      }
+      if constexpr (S % UPS == 0 && S / UPS >= 1 && S / UPS <= 16) {
+        constexpr int u = S / UPS - 1;
+        w[u] = pack_bf16x2(pe[u][0], pe[u][1]);
+      }
+      if constexpr (S % UPS == 0 && S / UPS >= 2 && S / UPS <= 17) {
+        constexpr int u = S / UPS - 2;
+        rs2[u % 4] = dot2_bf16_ones(w[u], rs2[u % 4]);  // row sum of the bf16 probabilities used
       }
       __builtin_amdgcn_sched_barrier(0);
     });
-    l_run += (rs2[0] + rs2[1]) + (rs2[2] + rs2[3]);
-    rescale(fmaxf(mxa, mxb), s_next);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // tiles it+1 (V) and it+2 (K) landed
-    __syncthreads();
-    s_cur[0] = s_next[0];
-    s_cur[1] = s_next[1];
+    l_tile = (rs2[0] + rs2[1]) + (rs2[2] + rs2[3]);
+    close_tile(s_cur, w);
+    if constexpr (NX) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // K(t+2) and V(t) landed
+      __syncthreads();
+      s_cur[0] = s_nx[0];
+      s_cur[1] = s_nx[1];
+    }
   };
-  // other head dims: the same work, ordered by the compiler
-  auto body_plain = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
-    constexpr int B = decltype(Bc)::value;
-    constexpr bool MN = decltype(Mc)::value;
-    if (it + 2 < nt) load_k(it + 2, Bc);
-    load_v(it + 1, std::integral_constant<int, B ^ 1>{});
-    f32x16 s_next[2];
-    scores(kbuf(std::integral_constant<int, B ^ 1>{}), s_next);
-    scale_half(s_next, 0);
-    scale_half(s_next, 1);
-    softmax_pv(s_cur, vbuf(Bc));
-    if (MN) mask(s_next, it + 1);
-    decide(s_next);
+
+  // regions [a, e) that have a successor and a predecessor, two at a time so that the
+  // buffer parity is a constant; MC: their tiles need the mask
+  auto run = [&](auto MCc, int a, int e) __attribute__((always_inline)) {
+    int it = a;
+    if ((it & 1) && it < e) region(std::integral_constant<int, 1>{}, std::true_type{}, std::true_type{}, MCc, it++);
+    for (; it + 1 < e; it += 2) {
+      region(std::integral_constant<int, 0>{}, std::true_type{}, std::true_type{}, MCc, it);
+      region(std::integral_constant<int, 1>{}, std::true_type{}, std::true_type{}, MCc, it + 1);
+    }
+    if (it < e) region(std::integral_constant<int, 0>{}, std::true_type{}, std::true_type{}, MCc, it);
+  };
+  // the last region (no successor): one instance for any parity, mask and predecessor,
+  // its two buffers chosen at run time (the compiler then waits for the in-flight load of
+  // V(t) before reading V(t-1) from the other buffer: once per workgroup)
+  auto last = [&](int it) __attribute__((always_inline)) {
+    if (it >= n_full) mask_tile(s_cur, it);
+    bf16* vld = (it & 1) ? sV1 : sV0;
+    const bf16* vt = (it & 1) ? sV0 : sV1;
+    dload(vbase + (long long)it * kBN * rs, vld);  // V(t) for the final products
+    uint32_t w[16];
+    float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      w[u] = expo_pair(s_cur, u);
+      if (u & 1) r1 = dot2_bf16_ones(w[u], r1); else r0 = dot2_bf16_ones(w[u], r0);
+    }
+    if (it > 0) {
+#pragma unroll
+      for (int q = 0; q < NP; ++q) {
+        const bf16x4 lo = lds_read_tr16(vt + 16 * (q / NDT) * D + voff[0][q % NDT]);
+        const bf16x4 up = lds_read_tr16(vt + 16 * (q / NDT) * D + voff[1][q % NDT]);
+        oacc[q % NDT] = mfma32(bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]}, pprev[q / NDT], oacc[q % NDT]);
+      }
+    }
+    l_tile = r0 + r1;
+    close_tile(s_cur, w);
+  };
+
+  if (nt > 0) {
+    // K(0) and K(1); the scores of tile 0
+    load_k(0, std::integral_constant<int, 0>{});
+    if (nt > 1) load_k(1, std::integral_constant<int, 1>{});
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    s_cur[0] = s_next[0];
-    s_cur[1] = s_next[1];
-  };
-  auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
-    if constexpr (D == 128)
-      body_sched(Bc, Mc, it);
-    else
-      body_plain(Bc, Mc, it);
-  };
-  // tiles [a, e) that have successors, two at a time so that B is a constant
-  auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
-    int it = a;
-    if ((it & 1) && it < e) body(std::integral_constant<int, 1>{}, Mc, it++);
-    for (; it + 1 < e; it += 2) {
-      body(std::integral_constant<int, 0>{}, Mc, it);
-      body(std::integral_constant<int, 1>{}, Mc, it + 1);
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      s_cur[mt] = mfma32(*(const bf16x8*)(sK0 + 32 * mt * D + koff[0]), qreg[0], zero16);
+#pragma unroll
+      for (int kk = 1; kk < NKK; ++kk) s_cur[mt] = mfma32(*(const bf16x8*)(sK0 + 32 * mt * D + koff[kk]), qreg[kk], s_cur[mt]);
     }
-    if (it < e) body(std::integral_constant<int, 0>{}, Mc, it);
-  };
-  if (nt > 0) {
-    const int split = max(0, min(nt - 1, n_full - 1));  // from here on tile it+1 is masked
-    run(std::false_type{}, 0, split);
-    run(std::true_type{}, split, nt - 1);
-    // last tile: no successor
-    if ((nt - 1) & 1)
-      softmax_pv(s_cur, sV1);
-    else
-      softmax_pv(s_cur, sV0);
+    // region 0 loads K(2) into the buffer of K(0): every wave must have read it
+    if (nt > 2) __syncthreads();
+    if (nt > 1) {
+      // region 0: no predecessor
+      region(std::integral_constant<int, 0>{}, std::true_type{}, std::false_type{}, std::false_type{}, 0, true);
+      const int split = max(1, min(nt - 1, n_full));  // regions from here on mask their tile
+      run(std::false_type{}, 1, split);
+      run(std::true_type{}, split, nt - 1);
+    }
+    last(nt - 1);
+    // O^T += V^T P^T of the last tile, from V(nt-1) in buffer (nt-1) % 2
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    const bf16* vt = ((nt - 1) & 1) ? sV1 : sV0;
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const bf16x4 lo = lds_read_tr16(vt + 16 * (q / NDT) * D + voff[0][q % NDT]);
+      const bf16x4 up = lds_read_tr16(vt + 16 * (q / NDT) * D + voff[1][q % NDT]);
+      oacc[q % NDT] = mfma32(bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]}, pprev[q / NDT], oacc[q % NDT]);
+    }
   }
 
   // ---- end of step: finalise or save the running state -------------------------------
+  // The per-lane indices are recomputed here from an opaque copy of the thread index, so
+  // that none of them is kept live (or spilled) across the tile loop.
+  int tid_e = threadIdx.x;
+  asm volatile("" : "+v"(tid_e));
+  const int lane_e = tid_e & 63, wave_e = tid_e >> 6, hi_e = lane_e >> 5;
+  const int qr_e = q_tile_row + wave_e * 32 + (lane_e & 31);
+  const long long st_row_e = (long long)bh * p.Sq + qr_e;
   const float l_tot = pair_sum(l_run);
   if (hs.flags & kLast) {
     const float inv = 1.f / l_tot;
-    bf16* orow = (bf16*)p.o + (long long)b * p.q_bstride + (long long)qr * rs + h * D;
+    bf16* orow = (bf16*)p.o + (long long)b * p.q_bstride + (long long)qr_e * rs + h * D;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d = 32 * dt + 8 * g + 4 * hi;
+        const int d = 32 * dt + 8 * g + 4 * hi_e;
         u32x2 w = {pack_bf16x2(oacc[dt][4 * g] * inv, oacc[dt][4 * g + 1] * inv),
                    pack_bf16x2(oacc[dt][4 * g + 2] * inv, oacc[dt][4 * g + 3] * inv)};
         *(u32x2*)(orow + d) = w;
       }
-    if (!hi) p.lse[st_row] = m_run * kLn2 + logf(l_tot);
+    if (!hi_e) p.lse[st_row_e] = m_run * kLn2 + logf(l_tot);
   } else {
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const f32x4 t = {oacc[dt][4 * g], oacc[dt][4 * g + 1], oacc[dt][4 * g + 2], oacc[dt][4 * g + 3]};
-        ((f32x4*)acc_tile)[((wave * NDT + dt) * 4 + g) * 64 + lane] = t;
+        ((f32x4*)acc_tile)[((wave_e * NDT + dt) * 4 + g) * 64 + lane_e] = t;
       }
-    if (!hi) {
-      p.m[st_row] = m_run;
-      p.l[st_row] = l_tot;
+    if (!hi_e) {
+      p.m[st_row_e] = m_run;
+      p.l[st_row_e] = l_tot;
     }
   }
 
@@ -479,14 +446,14 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
     u32x4 kx[PER], vx[PER];
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-      const int idx = e * kThreads + tid;
+      const int idx = e * kThreads + tid_e;
       const long long off = (long long)(qt * kBM + idx / CPR) * rs + 8 * (idx % CPR);
       kx[e] = *(const u32x4*)(kbase + off);
       vx[e] = *(const u32x4*)(vbase + off);
     }
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-      const int idx = e * kThreads + tid;
+      const int idx = e * kThreads + tid_e;
       const long long off = (long long)(qt * kBM + idx / CPR) * rs + 8 * (idx % CPR);
       *(u32x4*)(kdst + off) = kx[e];
       *(u32x4*)(vdst + off) = vx[e];

@@ -60,6 +60,16 @@ __device__ __forceinline__ void buffer_load_lds16(const void* base, int num_byte
 #endif
 }
 
+// As buffer_load_lds16, the read address being base + voff_bytes + soff_bytes with soff_bytes
+// wave-uniform (a scalar register: no vector register per load).
+__device__ __forceinline__ void buffer_load_lds16_so(const void* base, int num_bytes, void* lds_dst, int voff_bytes,
+                                                     int soff_bytes) {
+#if __HIP_DEVICE_COMPILE__
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, num_bytes, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)lds_dst, 16, voff_bytes, soff_bytes, 0, 0);
+#endif
+}
+
 // As buffer_load_lds16 with 4 bytes per lane (lane i lands at byte 4 i of lds_dst).
 __device__ __forceinline__ void buffer_load_lds4(const void* base, int num_bytes, void* lds_dst, int voff_bytes) {
 #if __HIP_DEVICE_COMPILE__
