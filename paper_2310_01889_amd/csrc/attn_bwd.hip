@@ -10,6 +10,7 @@
 // the host's query tiles) and one owning query tiles (dQ in registers, looping over the
 // block's key tiles).  Both write their tile once per step, so no atomics are needed.
 #include "ra_common.h"
+#include "ra_dma.h"
 #include "ra_kernels.h"
 
 namespace ra {
@@ -460,10 +461,14 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   constexpr int NKK = D / 16, NDT = D / 32, CPR = D / 8;
   constexpr int ROWS_PER_LOAD = 64 / CPR, LOADS = kKK / 4 / ROWS_PER_LOAD;
   // one LDS object per buffer (see the dK/dV kernel)
-  __shared__ __attribute__((aligned(1024))) bf16 sK0[kKK * D];
-  __shared__ __attribute__((aligned(1024))) bf16 sK1[kKK * D];
-  __shared__ __attribute__((aligned(1024))) bf16 sV0[kKK * D];
-  __shared__ __attribute__((aligned(1024))) bf16 sV1[kKK * D];
+  // one LDS array (K0, K1, V0, V1 tiles), filled by direct-to-LDS loads the compiler does
+  // not track (each tile's loads are waited for before the barrier that ends the tile), so
+  // that every read address is one register plus an immediate offset
+  __shared__ __attribute__((aligned(1024))) bf16 lds[4 * kKK * D];
+  bf16* const sK0 = lds;
+  bf16* const sK1 = lds + kKK * D;
+  bf16* const sV0 = lds + 2 * kKK * D;
+  bf16* const sV1 = lds + 3 * kKK * D;
   auto pick = [](auto Bc, auto* a, auto* b) __attribute__((always_inline)) {
     if constexpr (decltype(Bc)::value == 0) return a; else return b;
   };
@@ -517,19 +522,20 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   const bf16* kbase = (const bf16*)hs.k + (long long)b * hs.kv_bstride + h * D;
   const bf16* vbase = (const bf16*)hs.v + (long long)b * hs.kv_bstride + h * D;
 
-  // direct-to-LDS staging: load j of a wave fills rows wave*16 + j*ROWS_PER_LOAD + lane/CPR
-  int goff[LOADS];
-#pragma unroll
-  for (int j = 0; j < LOADS; ++j) {
-    const int r = wave * 16 + j * ROWS_PER_LOAD + lane / CPR;
-    goff[j] = 2 * (r * rs + 8 * ((lane % CPR) ^ swz<D>(r)));
-  }
+  // direct-to-LDS staging: load j of wave w fills rows j * 4 ROWS_PER_LOAD + w ROWS_PER_LOAD +
+  // lane / CPR.  The swizzle of those rows does not depend on j, so all loads of a lane read
+  // at one byte offset goff plus a wave-uniform j * 8 ROWS_PER_LOAD * rs bytes.
+  static_assert(16 == LOADS * ROWS_PER_LOAD, "each wave fills LOADS row groups");
+  const int goff = 2 * ((wave * ROWS_PER_LOAD + lane / CPR) * rs +
+                        8 * ((lane % CPR) ^ swz<D>(wave * ROWS_PER_LOAD + lane / CPR)));
   auto load_tile = [&](int it, auto Bc) __attribute__((always_inline)) {
     const long long t0 = (long long)it * kKK * rs;
+    const __amdgpu_buffer_rsrc_t rk = make_rsrc(kbase + t0, kKK * rs * 2), rv = make_rsrc(vbase + t0, kKK * rs * 2);
 #pragma unroll
     for (int j = 0; j < LOADS; ++j) {
-      buffer_load_lds16(kbase + t0, kKK * rs * 2, pick(Bc, sK0, sK1) + (wave_u * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
-      buffer_load_lds16(vbase + t0, kKK * rs * 2, pick(Bc, sV0, sV1) + (wave_u * 16 + j * ROWS_PER_LOAD) * D, goff[j]);
+      const int row = (j * 4 + wave_u) * ROWS_PER_LOAD, so = j * 8 * ROWS_PER_LOAD * rs;
+      dma_lds16_so(rk, lds_addr(pick(Bc, sK0, sK1) + row * D), goff, so);
+      dma_lds16_so(rv, lds_addr(pick(Bc, sV0, sV1) + row * D), goff, so);
     }
   };
   // row reads (A operand, rows 32 mt + swap_bits23(l32)) and transpose reads of the tiles
@@ -550,7 +556,86 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
   const float sl2 = p.scale * kLog2e;
   const float nl2 = nlse_s * sl2;  // -lse log2(e): the exponent is q.k sl2 + nl2 in float32
 
-  auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+  // One 64-key tile, laid out by hand in fenced steps: the S^T and dP^T products of the
+  // first 32 keys (the two chains alternating), then those of the last 32 keys while the
+  // first 32 keys' probabilities and dS are formed, then the 16 dQ^T products while the
+  // last 32 keys' dS are formed; operand reads PF steps ahead.
+  auto body_sched = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+    constexpr int B = decltype(Bc)::value;
+    constexpr bool MASK = decltype(Mc)::value;
+    if (it + 1 < nt) load_tile(it + 1, std::integral_constant<int, B ^ 1>{});
+    const bf16* kt = pick(Bc, sK0, sK1);
+    const bf16* vt = pick(Bc, sV0, sV1);
+    constexpr int NA = 2 * NKK;       // S^T and dP^T products of one 32-key half
+    constexpr int NQ = 4 * NDT;       // dQ^T products of the tile
+    constexpr int NST = 2 * NA + NQ;  // steps
+    constexpr int PF = 2;
+    f32x16 sacc[2], dpacc[2];
+    bf16x8 aop[2 * NA], top[NQ];
+    u32x4 w[4];  // dS^T of the four 16-key groups, packed bf16: the B operands as they are
+    const int kpos0 = hs.k_pos0 + it * kKK;
+    // step S < 2 NA: half h = S / NA, product j = S % NA of it (S^T if j even, dP^T if odd,
+    // reduction slice kk = j / 2); step S >= 2 NA: dQ^T product q = S - 2 NA (keys of group
+    // kb = q / NDT, dims 32 (q % NDT)..)
+    auto fetch = [&](auto Sc) __attribute__((always_inline)) {
+      constexpr int S = decltype(Sc)::value;
+      if constexpr (S < 2 * NA) {
+        constexpr int h = S / NA, j = S % NA, kk = j / 2;
+        aop[S] = *(const bf16x8*)(((j & 1) ? vt : kt) + 32 * h * D + roff[kk]);
+      } else {
+        constexpr int q = S - 2 * NA, kb = q / NDT, dt = q % NDT;
+        const bf16x4 lo = lds_read_tr16(kt + 16 * kb * D + toff[0][dt]);
+        const bf16x4 up = lds_read_tr16(kt + 16 * kb * D + toff[1][dt]);
+        top[q] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+      }
+    };
+    // pair jj of the 4 of key group kb: probabilities and dS, packed bf16
+    auto unit = [&](int kb, int jj) __attribute__((always_inline)) {
+      float ds2[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int i = 8 * (kb & 1) + 2 * jj + e;
+        const int mt = kb >> 1;
+        float pv = fast_exp2(fmaf(sacc[mt][i], sl2, nl2));
+        if (MASK) {
+          const int kpos = kpos0 + 32 * mt + 16 * (i >> 3) + 8 * hi + (i & 7);
+          if (kpos > qpos) pv = 0.f;
+        }
+        ds2[e] = pv * dpacc[mt][i];
+      }
+      w[kb][jj] = pack_bf16x2(ds2[0], ds2[1]);
+    };
+    // vector work: group kb's four pairs at steps VSTEP(kb) .. + 3 (groups 0, 1 once the
+    // first half's chains are complete, groups 2, 3 once the second half's are)
+    static_assert(NKK == 8 && NDT == 4, "hand schedule written for D = 128");
+    constexpr int V0 = NA + 2, V2 = 2 * NA;
+    static_for<0, PF>([&](auto Sc) __attribute__((always_inline)) { fetch(Sc); });
+    static_for<0, NST>([&](auto Sc) __attribute__((always_inline)) {
+      constexpr int S = decltype(Sc)::value;
+      if constexpr (S + PF < NST) fetch(std::integral_constant<int, S + PF>{});
+      if constexpr (S < 2 * NA) {
+        constexpr int h = S / NA, j = S % NA, kk = j / 2;
+        if constexpr (j == 1) {  // dP^T of half h starts at -Delta (set here: shorter live range)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) dpacc[h][i] = ndlt;
+        }
+        if constexpr (j & 1)
+          dpacc[h] = mfma32(aop[S], oreg[kk], dpacc[h]);
+        else
+          sacc[h] = mfma32(aop[S], qreg[kk], kk == 0 ? f32x16{} : sacc[h]);
+      } else {
+        constexpr int q = S - 2 * NA, kb = q / NDT, dt = q % NDT;
+        dqacc[dt] = mfma32(top[q], __builtin_bit_cast(bf16x8, w[kb]), dqacc[dt]);
+      }
+      if constexpr (S >= V0 && S < V0 + 8) unit((S - V0) / 4, (S - V0) % 4);
+      if constexpr (S >= V2 && S < V2 + 8) unit(2 + (S - V2) / 4, (S - V2) % 4);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  };
+  // other head dims: the same work, ordered by the compiler
+  auto body_plain = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
     constexpr int B = decltype(Bc)::value;
     constexpr bool MASK = decltype(Mc)::value;
     if (it + 1 < nt) load_tile(it + 1, std::integral_constant<int, B ^ 1>{});
@@ -602,6 +687,12 @@ __global__ __launch_bounds__(kBT, 2) void bwd_dq_bf16_kernel(const BwdStep p) {
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  };
+  auto body = [&](auto Bc, auto Mc, int it) __attribute__((always_inline)) {
+    if constexpr (D == 128)
+      body_sched(Bc, Mc, it);
+    else
+      body_plain(Bc, Mc, it);
   };
   auto run = [&](auto Mc, int a, int e) __attribute__((always_inline)) {
     int it = a;

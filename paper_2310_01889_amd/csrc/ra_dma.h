@@ -16,6 +16,12 @@ __device__ __forceinline__ void dma_lds16(const __amdgpu_buffer_rsrc_t& rsrc, un
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_addr), "v"(voff), "s"(rsrc)
                : "memory");
 }
+// As dma_lds16, the read address plus a wave-uniform byte offset soff (scalar register).
+__device__ __forceinline__ void dma_lds16_so(const __amdgpu_buffer_rsrc_t& rsrc, unsigned lds_addr, int voff, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(lds_addr), "v"(voff), "s"(rsrc),
+               "s"(soff)
+               : "memory");
+}
 __device__ __forceinline__ void dma_lds4(const __amdgpu_buffer_rsrc_t& rsrc, unsigned lds_addr, int voff) {
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds" ::"s"(lds_addr), "v"(voff), "s"(rsrc)
                : "memory");
