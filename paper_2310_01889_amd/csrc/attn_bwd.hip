@@ -70,9 +70,62 @@ __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const 
   }
 }
 
+// Adds a workgroup's dK (DK) or dV contribution (lanes over keys, accumulated transposed:
+// register 4 gg + e of product tile dt holds d = 32 dt + 8 gg + 4 hi + e) into the float32
+// gradient of the block (its home rows); dK carries the 1/sqrt(D).  The block's first
+// contribution is written, not added; its last goes out in bf16.  The sums are formed in
+// the accumulators, every carried value loaded before the first store.
+template <int NDT, bool DK>
+__device__ __forceinline__ void dkdv_epilogue(const BwdStep& p, int slot, int b, int h, int key_in_blk, int hi,
+                                                   f32x16 (&acc)[NDT]) {
+  constexpr int D = 32 * NDT;
+  const int rs = p.H * D;
+  const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key_in_blk) * rs + h * D;
+  const int kf = p.dkv_flags[slot];
+  float* g32 = DK ? p.dk : p.dv;
+  const float sc = DK ? p.scale : 1.f;
+  if (kf & kFirst) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[dt][i] = DK ? 0.f + acc[dt][i] * sc : 0.f + acc[dt][i];
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int d = 32 * dt + 8 * gg + 4 * hi;
+        const f32x4 c4 = *(const f32x4*)(g32 + grow + d);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[dt][4 * gg + e] = DK ? c4[e] + acc[dt][4 * gg + e] * sc : c4[e] + acc[dt][4 * gg + e];
+      }
+  }
+  if (kf & kLast) {
+    bf16* o16 = (bf16*)(DK ? p.dk_out : p.dv_out);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int d = 32 * dt + 8 * gg + 4 * hi;
+        const f32x16& a = acc[dt];
+        *(u32x2*)(o16 + grow + d) = u32x2{pack_bf16x2(a[4 * gg], a[4 * gg + 1]), pack_bf16x2(a[4 * gg + 2], a[4 * gg + 3])};
+      }
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) {
+        const int d = 32 * dt + 8 * gg + 4 * hi;
+        const f32x16& a = acc[dt];
+        *(f32x4*)(g32 + grow + d) = f32x4{a[4 * gg], a[4 * gg + 1], a[4 * gg + 2], a[4 * gg + 3]};
+      }
+  }
+}
+
 // =====================================================================================
-// bf16 dK/dV kernel: 4 waves x 32 keys = 128 keys per workgroup; loops over 32-query
-// tiles of the host's block.  Per wave, lanes run over the wave's keys:
+// bf16 dK/dV kernel (D = 64; D = 128 runs the split kernel below, whose waves hold the
+// same products): 4 waves x 32 keys = 128 keys per workgroup; loops over 32-query tiles
+// of the host's block.  Per wave, lanes run over the wave's keys:
 //   S' = Q K^T - lse sqrt(D)   [query x key] (A = Q rows from LDS with row bits 2 and 3
 //        swapped, B = K of the wave's keys in registers, as stored: the products are
 //        exact in float32; the accumulator starts at -lse sqrt(D) of its query)
@@ -388,61 +441,327 @@ __global__ __launch_bounds__(kBT, 1) void bwd_dkdv_bf16_kernel(const BwdStep p) 
     if (ql < qt_free) last(std::true_type{}); else last(std::false_type{});
   }
 
-  // add into the float32 gradient of the block (its home rows); dK carries the 1/sqrt(D).
-  // The block's first contribution is written, not added; its last goes out in bf16.
-  // Every carried value is loaded before the first store (the compiler cannot tell the dV
-  // loads from the dK stores, and would otherwise wait for one memory round trip per
-  // 16-byte piece).
-  const long long grow = (long long)b * p.dkv_bstride + (long long)(p.dkv_row0[slot] + key_in_blk) * rs + h * D;
-  const int kf = p.dkv_flags[slot];
-  f32x4 kin[NDT][4], vin[NDT][4];
-  if (kf & kFirst) {
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int gg = 0; gg < 4; ++gg) kin[dt][gg] = vin[dt][gg] = f32x4{0.f, 0.f, 0.f, 0.f};
-  } else {
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int gg = 0; gg < 4; ++gg) {
-        const int d = 32 * dt + 8 * gg + 4 * hi;
-        kin[dt][gg] = *(const f32x4*)(p.dk + grow + d);
-        vin[dt][gg] = *(const f32x4*)(p.dv + grow + d);
-      }
-  }
-#pragma unroll
-  for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-    for (int gg = 0; gg < 4; ++gg)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        kin[dt][gg][e] += dkacc[dt][4 * gg + e] * p.scale;
-        vin[dt][gg][e] += dvacc[dt][4 * gg + e];
-      }
-  if (kf & kLast) {
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int gg = 0; gg < 4; ++gg) {
-        const int d = 32 * dt + 8 * gg + 4 * hi;
-        const f32x4 k4 = kin[dt][gg], v4 = vin[dt][gg];
-        *(u32x2*)((bf16*)p.dk_out + grow + d) = u32x2{pack_bf16x2(k4[0], k4[1]), pack_bf16x2(k4[2], k4[3])};
-        *(u32x2*)((bf16*)p.dv_out + grow + d) = u32x2{pack_bf16x2(v4[0], v4[1]), pack_bf16x2(v4[2], v4[3])};
-      }
-  } else {
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int gg = 0; gg < 4; ++gg) {
-        const int d = 32 * dt + 8 * gg + 4 * hi;
-        *(f32x4*)(p.dk + grow + d) = kin[dt][gg];
-        *(f32x4*)(p.dv + grow + d) = vin[dt][gg];
-      }
-  }
+  dkdv_epilogue<NDT, true>(p, slot, b, h, key_in_blk, hi, dkacc);
+  dkdv_epilogue<NDT, false>(p, slot, b, h, key_in_blk, hi, dvacc);
 }
 
 // =====================================================================================
+// bf16 dK/dV kernel for D = 128 with the work of each 32-key column split over three
+// waves: 12 waves and 128 keys per workgroup, three waves on every SIMD.
+//   row wave (w < 4, column w): holds K and V of keys 32 w .. 32 w + 31 in registers and,
+//     per 32-query tile, runs the products contracted over D and the vector work
+//       S' = Q K^T - lse sqrt(D),  dP = dO V^T - Delta,
+//       P = exp2(S' log2e / sqrt(D)) (masked -> 0),  dS = P * dP,
+//     and stores P and dS, packed to bf16 in the lane order of a B operand, to LDS;
+//   dV wave (w = 4 + column), one tile later:  dV^T += dO^T P;
+//   dK wave (w = 8 + column), one tile later:  dK^T += Q^T dS
+//     (A operands by LDS transpose reads; each of the two holds 64 accumulator registers).
+// At 162 registers a wave, three waves share each SIMD: the row wave is mostly vector
+// work, the other two only matrix products and LDS reads, so each covers the others'
+// waits for LDS and for the barrier (with one wave per SIMD, as in the kernel above, those
+// waits leave the matrix core idle).  The operands and their order of accumulation are
+// those of the one-wave kernel, so the results are the same bit for bit.
+// Q and dO tiles (XOR-swizzled rows) with the tile's -lse sqrt(D) and -Delta stream by
+// direct-to-LDS loads (waves 0-7, 4 rows each) into a ring of four buffers: in the region
+// of tile t the row waves read tile t+1, the dV and dK waves tile t-1, and tile t+2 streams
+// in.  The packed P and dS pass through two exchange buffers; one barrier per tile.
+// =====================================================================================
+constexpr int kPT = 768;
+
+__global__ __launch_bounds__(kPT) void bwd_dkdv_split_kernel(const BwdStep p) {
+  constexpr int D = 128, NKK = D / 16, NDT = D / 32, CPR = D / 8, ROWS_PER_LOAD = 64 / CPR;
+  static_assert(kQB == 8 * ROWS_PER_LOAD, "waves 0-7 fill 4 rows of a tile each");
+  // Q tiles 0-3, then dO tiles 0-3, in one LDS object, so that every read of a ring buffer
+  // is one lane offset plus an immediate; filled by direct-to-LDS loads the compiler does
+  // not track (the region's explicit vmcnt wait and barrier order them)
+  __shared__ __attribute__((aligned(1024))) bf16 sQO[8 * kQB * D];
+  // -lse sqrt(D) of tiles 0-3, then -Delta: 64 floats each, as a one-wave 4-byte load
+  // writes 256 bytes (lanes past the tile read zero)
+  __shared__ __attribute__((aligned(1024))) float sLD[8 * 64];
+  // packed P and dS of a tile: [column][P of queries 0-15, 16-31, dS of 0-15, 16-31][lane]
+  __shared__ __attribute__((aligned(1024))) u32x4 sX0[4 * 4 * 64];
+  __shared__ __attribute__((aligned(1024))) u32x4 sX1[4 * 4 * 64];
+  auto qt_lds = [&](auto Bc) __attribute__((always_inline)) { return sQO + (decltype(Bc)::value % 4) * kQB * D; };
+  auto ot_lds = [&](auto Bc) __attribute__((always_inline)) { return sQO + (4 + decltype(Bc)::value % 4) * kQB * D; };
+  auto l_lds = [&](auto Bc) __attribute__((always_inline)) { return sLD + (decltype(Bc)::value % 4) * 64; };
+  auto d_lds = [&](auto Bc) __attribute__((always_inline)) { return sLD + (4 + decltype(Bc)::value % 4) * 64; };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+
+  const int n_kt = p.c / kKB;
+  const int BH = p.B * p.H;
+  const int total = p.n_slots * BH * n_kt;
+  const int Lid = xcd_swizzle(blockIdx.x, total);
+  const int grp = Lid / n_kt, kt = Lid % n_kt;
+  const int slot = grp / BH, bh = grp % BH;
+  const int b = bh / p.H, h = bh % p.H;
+  const StepHost hs = p.host[slot];
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS destinations in scalar registers
+  const int col = wave_u & 3;                                   // the wave's 32-key column
+  const int rs = p.H * D;
+  const int key_in_blk = kt * kKB + col * 32 + l32;  // this lane's key (B-operand column)
+
+  // query tiles with at least one query that sees a key of this workgroup; from
+  // qt_free on every query sees every key (no mask)
+  const int wg_first_k = hs.k_pos0 + kt * kKB;
+  const int n_qtiles = p.c / kQB;
+  int qt0 = 0, qt_free = 0;
+  if (p.causal) {
+    const int rel = wg_first_k - hs.q_pos0;
+    qt0 = rel <= 0 ? 0 : min(n_qtiles, rel / kQB);
+    const int rel_last = wg_first_k + kKB - 1 - hs.q_pos0;  // last key's offset in the q block
+    qt_free = rel_last < 0 ? 0 : min(n_qtiles, (rel_last + kQB - 1) / kQB);
+    qt_free = max(qt_free, qt0);
+  }
+  const int n = n_qtiles - qt0;  // tiles visited; tile i of the workgroup is query tile qt0 + i
+
+  const bf16* qbase = (const bf16*)p.q + (long long)b * p.q_bstride + h * D;
+  const bf16* obase = (const bf16*)p.dO + (long long)b * p.q_bstride + h * D;
+  const long long lrow0 = (long long)bh * p.Sq + hs.q_row0;
+  const int lrow = (wave_u & 7) * ROWS_PER_LOAD + lane / CPR;  // the tile row this lane fills (waves 0-7)
+  const int goff = 2 * (lrow * rs + 8 * ((lane % CPR) ^ swz<D>(lrow)));
+  // tile i into ring buffer buf: the Q and dO rows by waves 0-7, -lse sqrt(D) by wave 0,
+  // -Delta by wave 1
+  auto load_tile = [&](int i, int buf) __attribute__((always_inline)) {
+    const int qt = qt0 + i;
+    const long long t0 = (long long)(hs.q_row0 + qt * kQB) * rs;
+    if (wave_u < 8) {
+      dma_lds16(make_rsrc(qbase + t0, kQB * rs * 2), lds_addr(sQO + (buf * kQB + wave_u * ROWS_PER_LOAD) * D), goff);
+      dma_lds16(make_rsrc(obase + t0, kQB * rs * 2), lds_addr(sQO + ((4 + buf) * kQB + wave_u * ROWS_PER_LOAD) * D),
+                goff);
+    }
+    if (wave_u == 0) dma_lds4(make_rsrc(p.lse + lrow0 + qt * kQB, kQB * 4), lds_addr(sLD + buf * 64), 4 * lane);
+    if (wave_u == 1) dma_lds4(make_rsrc(p.delta + lrow0 + qt * kQB, kQB * 4), lds_addr(sLD + (4 + buf) * 64), 4 * lane);
+  };
+  // regions [a, e) with the buffer of region i (i % 4) known at compile time
+  auto run4 = [&](int a, int e, auto&& f) __attribute__((always_inline)) {
+    int i = a;
+    if (i < e && (i & 3) == 1) f(I1{}, i++);
+    if (i < e && (i & 3) == 2) f(I2{}, i++);
+    if (i < e && (i & 3) == 3) f(I3{}, i++);
+    for (; i + 3 < e; i += 4) {
+      f(I0{}, i);
+      f(I1{}, i + 1);
+      f(I2{}, i + 2);
+      f(I3{}, i + 3);
+    }
+    if (i < e) f(I0{}, i++);
+    if (i < e) f(I1{}, i++);
+    if (i < e) f(I2{}, i++);
+  };
+  auto at = [&](int i, auto&& f) __attribute__((always_inline)) {  // one region, buffer i % 4
+    switch (i & 3) {
+      case 0: f(I0{}, i); break;
+      case 1: f(I1{}, i); break;
+      case 2: f(I2{}, i); break;
+      default: f(I3{}, i); break;
+    }
+  };
+  auto sync = [&]() __attribute__((always_inline)) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's loads of tile i+2 landed
+    __syncthreads();                                   // every wave's; the exchange written
+  };
+
+  if (n > 0) {
+    load_tile(0, 0);
+    if (n > 1) load_tile(1, 1);
+  }
+
+  if (wave_u < 4) {
+    // ---------------------------------------------------------------- row wave
+    const int kpos = hs.k_pos0 + key_in_blk;
+    const float sl2 = p.scale * kLog2e;
+    const bf16* krow = (const bf16*)hs.k + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
+    const bf16* vrow = (const bf16*)hs.v + (long long)b * hs.kv_bstride + (long long)key_in_blk * rs + h * D;
+    // forwarding: the row waves write the rows of the workgroup's 128 keys, as loaded,
+    // into the next host's receive slot for the next ring step (layout [B, c, H, D])
+    const int fto = p.fwd.to[slot] - 1;  // destination slot, or -1
+    bf16* fkrow = nullptr;
+    bf16* fvrow = nullptr;
+    if (fto >= 0 && p.fwd.k0 != nullptr && p.fwd.v0 != nullptr) {
+      const long long off = (long long)fto * p.fwd.blk_bytes + 2 * (((long long)b * p.c + key_in_blk) * rs + h * D);
+      fkrow = (bf16*)((char*)p.fwd.k0 + off);
+      fvrow = (bf16*)((char*)p.fwd.v0 + off);
+    }
+    bf16x8 kreg[NKK], vreg[NKK];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      const bf16x8 kx = *(const bf16x8*)(krow + 16 * kk + 8 * hi);
+      vreg[kk] = *(const bf16x8*)(vrow + 16 * kk + 8 * hi);
+      if (fkrow) {
+        *(bf16x8*)(fkrow + 16 * kk + 8 * hi) = kx;
+        *(bf16x8*)(fvrow + 16 * kk + 8 * hi) = vreg[kk];
+      }
+      kreg[kk] = kx;
+    }
+    if (n == 0) return;
+    const int qrow = swap_bits23(l32);
+    int roff[NKK];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) roff[kk] = qrow * D + 8 * ((2 * kk + hi) ^ swz<D>(qrow));
+    // accumulator starts of S' (-lse sqrt(D)) and dP (-Delta) of a tile: register 8 g + e
+    // of a lane holds query 16 g + 8 hi + e
+    auto inits = [&](auto Bc, f32x16& si, f32x16& di) __attribute__((always_inline)) {
+      const float* sl = l_lds(Bc);
+      const float* sd = d_lds(Bc);
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const int q0 = 16 * g + 8 * hi;
+        const f32x4 la = *(const f32x4*)&sl[q0], lb = *(const f32x4*)&sl[q0 + 4];
+        const f32x4 da = *(const f32x4*)&sd[q0], db = *(const f32x4*)&sd[q0 + 4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          si[8 * g + e] = la[e];
+          si[8 * g + 4 + e] = lb[e];
+          di[8 * g + e] = da[e];
+          di[8 * g + 4 + e] = db[e];
+        }
+      }
+    };
+    // P and dS (bf16 pairs) of group g (16 queries) of a tile, pair u of the group's 4
+    auto unit = [&](auto Mc, const f32x16& sc, const f32x16& dpc, int qpos0, int g, int u, uint32_t& w1,
+                    uint32_t& w2) __attribute__((always_inline)) {
+      constexpr bool MASK = decltype(Mc)::value;
+      float pv[2], dsv[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int r = 8 * g + 2 * u + e;
+        float pr = fast_exp2(sc[r] * sl2);
+        if (MASK && kpos > qpos0 + 16 * g + 8 * hi + 2 * u + e) pr = 0.f;
+        pv[e] = pr;
+        dsv[e] = pr * dpc[r];
+      }
+      w1 = pack_bf16x2(pv[0], pv[1]);
+      w2 = pack_bf16x2(dsv[0], dsv[1]);
+    };
+    sync();
+    f32x16 s_cur, dp_cur;  // S' and dP of the tile whose P and dS are formed next
+    inits(I0{}, s_cur, dp_cur);
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      s_cur = mfma32(*(const bf16x8*)(qt_lds(I0{}) + roff[kk]), kreg[kk], s_cur);
+      dp_cur = mfma32(*(const bf16x8*)(ot_lds(I0{}) + roff[kk]), vreg[kk], dp_cur);
+    }
+    // Region of tile i (buffer Bc; Nc: tile i+1 exists): loads of tile i+2, the S'/dP
+    // products of tile i+1 in 16 fenced steps (S' and dP alternate; operand reads two
+    // steps ahead), and P, dS of tile i, one pair unit at every even step; each group's
+    // packed P and dS go to the exchange buffer of tile i once formed.
+    auto region = [&](auto Bc, auto Mc, auto Nc, int i) __attribute__((always_inline)) {
+      constexpr int B = decltype(Bc)::value;
+      constexpr bool NX = decltype(Nc)::value;
+      using Bn = std::integral_constant<int, (B + 1) % 4>;
+      using Bl = std::integral_constant<int, (B + 2) % 4>;
+      if (i + 2 < n) load_tile(i + 2, Bl::value);
+      const bf16* qn = qt_lds(Bn{});
+      const bf16* on = ot_lds(Bn{});
+      u32x4* xw = ((B & 1) ? sX1 : sX0) + col * 4 * 64 + lane;
+      const int qpos0 = hs.q_pos0 + (qt0 + i) * kQB;
+      f32x16 s_nx, dp_nx;
+      if constexpr (NX) inits(Bn{}, s_nx, dp_nx);
+      bf16x8 aop[16];
+      uint32_t wp[2][4], ws[2][4];
+      constexpr int kPF = 2;
+      auto read_a = [&](auto Sc) __attribute__((always_inline)) {  // product s: kk = s / 2, dP if odd
+        constexpr int S = decltype(Sc)::value;
+        aop[S] = *(const bf16x8*)(((S & 1) ? on : qn) + roff[S / 2]);
+      };
+      if constexpr (NX) static_for<0, kPF>([&](auto Sc) __attribute__((always_inline)) { read_a(Sc); });
+      static_for<0, 16>([&](auto Sc) __attribute__((always_inline)) {
+        constexpr int S = decltype(Sc)::value;
+        if constexpr (NX && S + kPF < 16) read_a(std::integral_constant<int, S + kPF>{});
+        if constexpr (NX) {
+          if constexpr (S & 1)
+            dp_nx = mfma32(aop[S], vreg[S / 2], dp_nx);
+          else
+            s_nx = mfma32(aop[S], kreg[S / 2], s_nx);
+        }
+        if constexpr (S % 2 == 0) {
+          constexpr int g = S / 8, u = (S % 8) / 2;
+          unit(Mc, s_cur, dp_cur, qpos0, g, u, wp[g][u], ws[g][u]);
+        }
+        if constexpr (S % 8 == 7) {
+          constexpr int g = S / 8;
+          xw[g * 64] = u32x4{wp[g][0], wp[g][1], wp[g][2], wp[g][3]};
+          xw[(2 + g) * 64] = u32x4{ws[g][0], ws[g][1], ws[g][2], ws[g][3]};
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      sync();
+      if constexpr (NX) {
+        s_cur = s_nx;
+        dp_cur = dp_nx;
+      }
+    };
+    // masked tiles first; every tile but the last has a successor
+    const int ms = max(0, min(qt_free - qt0, n - 1));
+    run4(0, ms, [&](auto Bc, int i) __attribute__((always_inline)) {
+      region(Bc, std::true_type{}, std::true_type{}, i);
+    });
+    run4(ms, n - 1, [&](auto Bc, int i) __attribute__((always_inline)) {
+      region(Bc, std::false_type{}, std::true_type{}, i);
+    });
+    if (qt0 + n - 1 < qt_free)
+      at(n - 1, [&](auto Bc, int i) __attribute__((always_inline)) { region(Bc, std::true_type{}, std::false_type{}, i); });
+    else
+      at(n - 1, [&](auto Bc, int i) __attribute__((always_inline)) { region(Bc, std::false_type{}, std::false_type{}, i); });
+    return;
+  }
+
+  // ------------------------------------------------------------------ column waves
+  // waves 4-7 accumulate dV, waves 8-11 dK, of the column
+  auto column = [&](auto Kc) __attribute__((always_inline)) {
+    constexpr bool DK = decltype(Kc)::value;
+    f32x16 acc[NDT];
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[dt][i] = 0.f;
+    if (n > 0) {
+      const int g16 = lane >> 4, li = lane & 15;
+      int toff[2][NDT];
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const int row = 8 * hi + 4 * r + (li >> 2);
+          const int d = 32 * dt + 16 * (g16 & 1) + 4 * (li & 3);
+          toff[r][dt] = row * D + 8 * ((d >> 3) ^ swz<D>(row)) + (d & 7);
+        }
+      sync();
+      for (int i = 0; i <= n; ++i) {
+        if (i + 2 < n) load_tile(i + 2, (i + 2) & 3);
+        if (i >= 1) {
+          const u32x4* xr = (((i - 1) & 1) ? sX1 : sX0) + col * 4 * 64 + lane + (DK ? 128 : 0);
+          const bf16x8 bop[2] = {__builtin_bit_cast(bf16x8, xr[0]), __builtin_bit_cast(bf16x8, xr[64])};
+          const bf16* src = sQO + ((DK ? 0 : 4) + ((i - 1) & 3)) * kQB * D;
+          bf16x8 top[8];
+          constexpr int kPF = 2;
+          auto read_t = [&](auto Qc) __attribute__((always_inline)) {  // product q: group q / 4, dt q % 4
+            constexpr int Q = decltype(Qc)::value, g = Q / 4, dt = Q % 4;
+            const bf16x4 lo = lds_read_tr16(src + 16 * g * D + toff[0][dt]);
+            const bf16x4 up = lds_read_tr16(src + 16 * g * D + toff[1][dt]);
+            top[Q] = bf16x8{lo[0], lo[1], lo[2], lo[3], up[0], up[1], up[2], up[3]};
+          };
+          static_for<0, kPF>([&](auto Qc) __attribute__((always_inline)) { read_t(Qc); });
+          static_for<0, 8>([&](auto Qc) __attribute__((always_inline)) {
+            constexpr int Q = decltype(Qc)::value, g = Q / 4, dt = Q % 4;
+            if constexpr (Q + kPF < 8) read_t(std::integral_constant<int, Q + kPF>{});
+            acc[dt] = mfma32(top[Q], bop[g], acc[dt]);
+            __builtin_amdgcn_sched_barrier(0);
+          });
+        }
+        if (i < n) sync();
+      }
+    }
+    dkdv_epilogue<NDT, DK>(p, slot, b, h, key_in_blk, hi, acc);
+  };
+  if (wave_u >= 8) column(std::true_type{});
+  else column(std::false_type{});
+}
+
 // bf16 dQ kernel: 4 waves x 32 queries = 128 queries per workgroup; loops over 64-key
 // tiles of the block.  Per wave, lanes run over queries:
 //   S^T  = K Q^T            (A = K rows from LDS, B = Q in registers)
@@ -930,7 +1249,7 @@ hipError_t launch_bwd_bf16(const BwdStep& s, int D, hipStream_t st) {
   const int g1 = s.n_slots * s.B * s.H * (s.c / kKB);
   const int g2 = s.n_slots * s.B * s.H * (s.c / kQQ);
   if (D == 128) {
-    hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<128>, dim3(g1), dim3(kBT), 0, st, s);
+    hipLaunchKernelGGL(bwd_dkdv_split_kernel, dim3(g1), dim3(kPT), 0, st, s);
     hipLaunchKernelGGL(bwd_dq_bf16_kernel<128>, dim3(g2), dim3(kBT), 0, st, s);
   } else {
     hipLaunchKernelGGL(bwd_dkdv_bf16_kernel<64>, dim3(g1), dim3(kBT), 0, st, s);
