@@ -35,32 +35,60 @@ constexpr int kLoadsPerTile = kTileB / 1024 / (kGT / 64);  // 1 KB loads per wav
 __device__ __forceinline__ int swz_row(int r) { return (r >> 2) & 3; }
 __device__ __forceinline__ int swz_kmaj(int r) { return 4 * (r & 3); }
 
+// sigmoid(u); silu(u) = u sigmoid(u) has derivative sigmoid(u) (1 + u (1 - sigmoid(u)))
+// (SwiGLU gate)
+__device__ __forceinline__ float sigmoid_f(float u) { return __builtin_amdgcn_rcpf(1.f + __expf(-u)); }
+
+// Exact GeLU h Phi(h) and Phi(h), phi(h) (standard normal CDF and density) from the erfc
+// approximation of Abramowitz and Stegun, formula 7.1.26: with a = |h| / sqrt(2),
+//   0.5 erfc(a) = Phi(-|h|) ~ t (b1 + t (b2 + t (b3 + t (b4 + t b5)))) exp(-a^2),
+//   t = 1 / (1 + p a), p = 0.3275911, b_i half the published a_i
+// (absolute error below 1.5e-7 in erf).  The lower tail is formed directly, without the
+// cancellation of 1 + erf for negative h; one reciprocal and one exponential, a third of
+// the instructions of a library erf in the epilogue.
+__device__ __forceinline__ float gauss_lower(float h, float& e) {  // Phi(-|h|); e = exp(-h^2 / 2)
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f * 0.7071067811865476f, fabsf(h), 1.f));
+  e = fast_exp2(h * (h * (-0.5f * kLog2e)));
+  const float poly =
+      t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 0.5307027145f, -0.7265760135f), 0.7107068705f), -0.142248368f), 0.127414796f);
+  return poly * e;
+}
+__device__ __forceinline__ float gelu_erf(float h) {
+  float e;
+  const float hl = h * gauss_lower(h, e);
+  return h >= 0.f ? h - hl : hl;
+}
+__device__ __forceinline__ float gauss_cdf(float h, float& pdf) {
+  float e;
+  const float lower = gauss_lower(h, e);
+  pdf = 0.3989422804014327f * e;
+  return h >= 0.f ? 1.f - lower : lower;
+}
+
 template <int ACT>
 __device__ __forceinline__ float act_apply(float h) {
   constexpr int act = ACT;
   if (act == 1) return fmaxf(h, 0.f);
-  if (act == 2) {
+  if (act == 2) {  // 0.5 (1 + tanh(u)) = sigmoid(2 u)
     const float u = 0.7978845608028654f * (h + 0.044715f * h * h * h);
-    return 0.5f * h * (1.f + tanhf(u));
+    return h * sigmoid_f(2.f * u);
   }
-  return 0.5f * h * (1.f + erff(h * 0.7071067811865476f));
+  return gelu_erf(h);
 }
 
-// silu(u) = u sigmoid(u) and its derivative sigmoid(u) (1 + u (1 - sigmoid(u))) (SwiGLU gate)
-__device__ __forceinline__ float sigmoid_f(float u) { return __builtin_amdgcn_rcpf(1.f + __expf(-u)); }
 
 template <int ACT>
 __device__ __forceinline__ float act_grad(float h) {
   constexpr int act = ACT;
   if (act == 1) return h > 0.f ? 1.f : 0.f;
-  if (act == 2) {
+  if (act == 2) {  // with s = sigmoid(2 u): 0.5 (1 + tanh u) = s, 0.5 (1 - tanh^2 u) = 2 s (1 - s)
     const float u = 0.7978845608028654f * (h + 0.044715f * h * h * h);
-    const float t = tanhf(u);
+    const float sg = sigmoid_f(2.f * u);
     const float du = 0.7978845608028654f * (1.f + 3.f * 0.044715f * h * h);
-    return 0.5f * (1.f + t) + 0.5f * h * (1.f - t * t) * du;
+    return sg + 2.f * h * sg * (1.f - sg) * du;
   }
-  const float cdf = 0.5f * (1.f + erff(h * 0.7071067811865476f));
-  const float pdf = 0.3989422804014327f * expf(-0.5f * h * h);
+  float pdf;
+  const float cdf = gauss_cdf(h, pdf);
   return cdf + h * pdf;
 }
 
