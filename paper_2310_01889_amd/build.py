@@ -43,7 +43,9 @@ def build(verbose=False, extra=()):
             if o.strip():
                 print(o)
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs
+    # --no-undefined: a symbol no object defines (e.g. a kernel's host stub that a
+    # translation unit failed to emit) fails the link here, not the first load on a GPU
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,--no-undefined", "-o", tmp] + objs
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout)
