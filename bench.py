@@ -13,8 +13,9 @@ the timed region.  Prints ONE JSON line.
 masking halves the diagonal blocks and skips blocks above the diagonal).  The
 `roofline` object reports the step kernel's own throughput (HIP events around every
 launch, on the stream it runs on) against the bf16 dense matrix-core peak, and beside it
-against the rate the chip sustains on back-to-back matrix products alone (the library's
-calibration kernel, measured in the same run).  `ms_per_step` is the mean over the timed
+against the rates the chip sustains on back-to-back matrix products alone (the library's
+calibration kernel, measured in the same run): with fixed operands, and with random
+operands that change from product to product as real data does.  `ms_per_step` is the mean over the timed
 calls, with their median and minimum alongside.  The
 `cpu_baseline` object times the blockwise fp64 ring oracle (torch CPU) on one head of the
 same workload and scales it to all 32 heads.  `extra` holds secondary configurations
@@ -80,19 +81,21 @@ def time_calls_each(fn, steps):
     return sum(per) / steps, statistics.median(per), min(per), wall
 
 
-def mfma_loop_peak(ra, torch, iters=3000, reps=5):
+def mfma_loop_peak(ra, torch, random_operands=False, iters=30000, reps=5):
     """Matrix-core throughput the chip sustains with nothing else running (the library's
     calibration kernel: 2048 waves of independent bf16 32x32x16 product chains), TFLOP/s,
-    median of `reps` timed launches."""
+    median of `reps` timed launches of ~25-40 ms.  random_operands=False: the same operands
+    in every product; True: random operands that change from product to product, as real
+    data does (the board then sustains a lower clock)."""
     import statistics
     for _ in range(2):
-        ra.mfma_probe(iters)
+        ra.mfma_probe(iters, random_operands)
     torch.cuda.synchronize()
     rates = []
     for _ in range(reps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        fl = ra.mfma_probe(iters)
+        fl = ra.mfma_probe(iters, random_operands)
         e1.record()
         torch.cuda.synchronize()
         rates.append(fl / (e0.elapsed_time(e1) * 1e-3) / 1e12)
@@ -368,6 +371,7 @@ def main():
     achieved = flops_per_launch / (k_avg_ms * 1e-3) / 1e12
     value = flops / (ms * 1e-3) / 1e12
     mfma_loop = mfma_loop_peak(ra, torch)
+    mfma_loop_rand = mfma_loop_peak(ra, torch, random_operands=True)
 
     out = {
         "metric": METRIC,
@@ -394,7 +398,9 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
                      "avg_launch_ms": round(k_avg_ms, 4), "launches": launches,
                      "mfma_loop_measured": round(mfma_loop, 1),
-                     "frac_of_mfma_loop": round(achieved / mfma_loop, 4)},
+                     "frac_of_mfma_loop": round(achieved / mfma_loop, 4),
+                     "mfma_loop_random_operands_measured": round(mfma_loop_rand, 1),
+                     "frac_of_mfma_loop_random_operands": round(achieved / mfma_loop_rand, 4)},
     }
 
     if not args.no_extra:

@@ -382,10 +382,13 @@ int ring_attn_timing_read(int kind, double* total_ms, int* launches);
  * iters x 32 bf16 32x32x16 matrix products (4 independent accumulator chains) and writes
  * one float to sink[wave].  The caller times the launch on `stream`: the work is
  * 2048 * iters * 32 * 32768 flop.
- *   iters  in [1, 2^20] (else RA_EINVAL)
- *   sink   device float[2048], overwritten
+ *   iters            in [1, 2^20] (else RA_EINVAL)
+ *   random_operands  0: the same two operands in every product (the headline rate);
+ *                    1: random signs and mantissas (magnitudes in [0.5, 8)) that change
+ *                    from one product to the next, as real data does (else RA_EINVAL)
+ *   sink             device float[2048], overwritten
  */
-int ring_attn_mfma_probe(int iters, float* sink, hipStream_t stream);
+int ring_attn_mfma_probe(int iters, int random_operands, float* sink, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -35,7 +35,7 @@ _LIB = None
 _P = ctypes.c_void_p
 _I = ctypes.c_int
 _SIGS = {
-    "ring_attn_mfma_probe": [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p],
+    "ring_attn_mfma_probe": [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p],
     "ring_attn_release_workspace": [],
     "ring_attn_fwd": [_P] * 5 + [_I] * 6 + [_P],
     "ring_attn_fwd_f32": [_P] * 5 + [_I] * 6 + [_P],
@@ -135,12 +135,13 @@ def release_workspace():
 MFMA_PROBE_WAVES = 2048
 
 
-def mfma_probe(iters, stream=None):
+def mfma_probe(iters, random_operands=False, stream=None):
     """Launch the matrix-core calibration kernel (ring_attn_mfma_probe) on the current
-    stream; returns the flops it performs.  Time it with events around the call."""
+    stream, with fixed or random operands; returns the flops it performs.  Time it with
+    events around the call."""
     import torch
     sink = torch.empty(MFMA_PROBE_WAVES, dtype=torch.float32, device="cuda")
-    _call("ring_attn_mfma_probe", int(iters), sink.data_ptr(), _stream(stream))
+    _call("ring_attn_mfma_probe", int(iters), 1 if random_operands else 0, sink.data_ptr(), _stream(stream))
     return float(MFMA_PROBE_WAVES) * iters * 32 * 32768
 
 

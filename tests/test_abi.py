@@ -149,7 +149,9 @@ def test_product_path_does_not_use_the_oracle():
 
 
 def test_mfma_probe_argument_validation(lib):
-    assert lib.ring_attn_mfma_probe(1, NULL, NULL) == RA_EINVAL
-    assert lib.ring_attn_mfma_probe(0, FAKE, NULL) == RA_EINVAL
-    assert lib.ring_attn_mfma_probe((1 << 20) + 1, FAKE, NULL) == RA_EINVAL
+    assert lib.ring_attn_mfma_probe(1, 0, NULL, NULL) == RA_EINVAL
+    assert lib.ring_attn_mfma_probe(0, 0, FAKE, NULL) == RA_EINVAL
+    assert lib.ring_attn_mfma_probe((1 << 20) + 1, 1, FAKE, NULL) == RA_EINVAL
     assert b"iters" in lib.ring_attn_last_error()
+    assert lib.ring_attn_mfma_probe(1, 2, FAKE, NULL) == RA_EINVAL
+    assert b"random_operands" in lib.ring_attn_last_error()
