@@ -18,7 +18,8 @@
 namespace ra {
 
 // ===================================================================================
-// bf16 kernel: 4 waves, 128 queries per workgroup (32 per wave), 64-key tiles.
+// bf16 kernel: NW = 4 or 8 waves, 32 queries per wave (128 or 256 per workgroup), 64-key
+// tiles.
 //
 // Per wave, scores are formed transposed, S^T = K Q^T (32x32x16 MFMA, A = K rows from
 // LDS, B = Q held in registers), so that each lane owns one query: its row max and
@@ -43,13 +44,15 @@ constexpr float kSumMax = 65536.f;  // overflow test: a lane's row sum over a ti
 // bit 2 flipped on odd s.  Tiles are filled with direct-to-LDS loads (no registers):
 // lane i of a 1 KB load lands at byte 16 i of its destination, so each lane fetches the
 // logical chunk that the swizzle puts there.
-template <int D>
-__global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) {
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) void fwd_bf16_kernel(const FwdStep p) {
+  constexpr int BM = 32 * NW;  // queries per workgroup (32 per wave)
+  constexpr int NT = 64 * NW;  // threads per workgroup
   constexpr int NKK = D / 16;  // 16-wide reduction steps of q.k
   constexpr int NDT = D / 32;  // 32-row output tiles of O^T
   constexpr int CPR = D / 8;   // 16-byte chunks per row
   constexpr int ROWS_PER_LOAD = 64 / CPR;               // rows filled by one 1 KB wave load
-  constexpr int RPW = kBN / 4;                           // tile rows each wave fills
+  constexpr int RPW = kBN / NW;                          // tile rows each wave fills
   constexpr int LOADS = RPW / ROWS_PER_LOAD;             // 1 KB loads per wave per tile
   constexpr int TILE = kBN * D;                          // elements per tile
   // Four separate LDS objects (not one [2][TILE] array per operand): the compiler then
@@ -68,7 +71,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
 
-  const int n_qt = p.c / kBM;
+  const int n_qt = p.c / BM;
   const int BH = p.B * p.H;
   const int total = p.n_slots * BH * n_qt;
   const int L = xcd_swizzle(blockIdx.x, total);
@@ -83,10 +86,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   const int l32 = lane & 31, hi = lane >> 5;
   const int rs = p.H * D;  // row stride of q / k / v / o (elements)
 
-  const int q_tile_row = hs.q_row0 + qt * kBM;       // first q-space row of the workgroup
+  const int q_tile_row = hs.q_row0 + qt * BM;       // first q-space row of the workgroup
   const int qr = q_tile_row + wave * 32 + l32;       // this lane's query row
-  const int qpos = hs.q_pos0 + qt * kBM + wave * 32 + l32;
-  const int tile_first_q = hs.q_pos0 + qt * kBM;
+  const int qpos = hs.q_pos0 + qt * BM + wave * 32 + l32;
+  const int tile_first_q = hs.q_pos0 + qt * BM;
 
   const bf16* qbase = (const bf16*)p.q + (long long)b * p.q_bstride + h * D;
   const bf16* kbase = (const bf16*)hs.k + (long long)b * hs.kv_bstride + h * D;
@@ -95,7 +98,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   // key tiles with at least one visible key; the first n_full need no mask
   int nt = p.c / kBN, n_full = nt;
   if (p.causal) {
-    const int vis = tile_first_q + kBM - hs.k_pos0;  // keys visible to the last row
+    const int vis = tile_first_q + BM - hs.k_pos0;  // keys visible to the last row
     nt = min(nt, max(0, (vis + kBN - 1) / kBN));
     n_full = min(nt, max(0, (tile_first_q - hs.k_pos0 + 1) / kBN));
   }
@@ -104,7 +107,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   f32x16 oacc[NDT];
   float m_run, l_run;
   const long long st_row = (long long)bh * p.Sq + qr;
-  float* acc_tile = p.acc + ((long long)bh * (p.Sq / kBM) + q_tile_row / kBM) * (kBM * D);
+  float* acc_tile = p.acc + ((long long)bh * (p.Sq / BM) + q_tile_row / BM) * (BM * D);
   if (hs.flags & kFirst) {
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -148,11 +151,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   const f32x16 zero16 = {};
 
   // ---- direct-to-LDS staging: each wave fills RPW rows of a tile ---------------------
-  // load j of wave w covers rows j * 4 ROWS_PER_LOAD + w ROWS_PER_LOAD + lane / CPR; the
+  // load j of wave w covers rows j * NW ROWS_PER_LOAD + w ROWS_PER_LOAD + lane / CPR; the
   // lane's physical chunk is lane % CPR, its logical (global) chunk that ^ swz(row).  With
   // rows interleaved over the waves this way, swz(row) is the same for all loads of a lane
   // (the row bits it reads do not depend on j), so every load of the lane reads at one
-  // byte offset goff plus a wave-uniform j * 8 ROWS_PER_LOAD * rs bytes.
+  // byte offset goff plus a wave-uniform j * 2 NW ROWS_PER_LOAD * rs bytes.
   static_assert(RPW == LOADS * ROWS_PER_LOAD, "each wave fills LOADS row groups");
   const int goff = 2 * ((wave * ROWS_PER_LOAD + lane / CPR) * rs +
                         8 * ((lane % CPR) ^ swz<D>(wave * ROWS_PER_LOAD + lane / CPR)));
@@ -161,8 +164,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   auto dload = [&](const bf16* src_tile, bf16* dst_tile) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < LOADS; ++j)
-      buffer_load_lds16_so(src_tile, kBN * rs * 2, dst_tile + (j * 4 + wave_u) * ROWS_PER_LOAD * D, goff,
-                           j * 8 * ROWS_PER_LOAD * rs);
+      buffer_load_lds16_so(src_tile, kBN * rs * 2, dst_tile + (j * NW + wave_u) * ROWS_PER_LOAD * D, goff,
+                           j * 2 * NW * ROWS_PER_LOAD * rs);
   };
   auto load_k = [&](int it, auto Bc) __attribute__((always_inline)) { dload(kbase + (long long)it * kBN * rs, kbuf(Bc)); };
   auto load_v = [&](int it, auto Bc) __attribute__((always_inline)) { dload(vbase + (long long)it * kBN * rs, vbuf(Bc)); };
@@ -439,22 +442,22 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(const FwdStep p) 
   // as they finish instead of by copies between the steps)
   const int fto = p.fwd.to[slot] - 1;  // destination slot, or -1
   if (fto >= 0 && p.fwd.k0 != nullptr && p.fwd.v0 != nullptr) {
-    constexpr int PER = kBM * CPR / kThreads;  // 16-byte chunks per thread per operand
+    constexpr int PER = BM * CPR / NT;  // 16-byte chunks per thread per operand
     const long long doff = (long long)fto * p.fwd.blk_bytes + 2 * ((long long)b * p.c * rs + h * D);
     bf16* kdst = (bf16*)((char*)p.fwd.k0 + doff);
     bf16* vdst = (bf16*)((char*)p.fwd.v0 + doff);
     u32x4 kx[PER], vx[PER];
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-      const int idx = e * kThreads + tid_e;
-      const long long off = (long long)(qt * kBM + idx / CPR) * rs + 8 * (idx % CPR);
+      const int idx = e * NT + tid_e;
+      const long long off = (long long)(qt * BM + idx / CPR) * rs + 8 * (idx % CPR);
       kx[e] = *(const u32x4*)(kbase + off);
       vx[e] = *(const u32x4*)(vbase + off);
     }
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
-      const int idx = e * kThreads + tid_e;
-      const long long off = (long long)(qt * kBM + idx / CPR) * rs + 8 * (idx % CPR);
+      const int idx = e * NT + tid_e;
+      const long long off = (long long)(qt * BM + idx / CPR) * rs + 8 * (idx % CPR);
       *(u32x4*)(kdst + off) = kx[e];
       *(u32x4*)(vdst + off) = vx[e];
     }
@@ -562,17 +565,27 @@ __global__ __launch_bounds__(64) void fwd_f32_kernel(const FwdStep p) {
 
 }  // namespace
 
+// Long blocks (D = 128, at least 16384 keys, a multiple of 256) run the eight-wave kernel:
+// 256 queries per workgroup, so each key/value tile is loaded once for twice the queries
+// (one workgroup per CU instead of two; at 4096-8192 keys the longer start and end of each
+// workgroup outweigh the saved loads).  The choice depends only on (D, c), so every step
+// of a call uses the same kernel and the float32 state keeps one layout.
+static bool fwd_bf16_wide(int D, int c) { return D == 128 && c % 256 == 0 && c >= 16384; }
+
 hipError_t launch_fwd_bf16(const FwdStep& s, int D, hipStream_t st) {
   const int total = s.n_slots * s.B * s.H * (s.c / kBM);
   if (total == 0) return hipSuccess;
+  const bool wide = fwd_bf16_wide(D, s.c);
   // a forwarding destination needs both receive bases and a slot size
   for (int n = 0; n < s.n_slots; ++n)
     if (s.fwd.to[n] != 0 && (s.fwd.to[n] < 0 || s.fwd.k0 == nullptr || s.fwd.v0 == nullptr || s.fwd.blk_bytes <= 0))
       return hipErrorInvalidValue;
-  if (D == 128)
-    hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3(total), dim3(kThreads), 0, st, s);
+  if (wide)
+    hipLaunchKernelGGL((fwd_bf16_kernel<128, 8>), dim3(total / 2), dim3(512), 0, st, s);
+  else if (D == 128)
+    hipLaunchKernelGGL((fwd_bf16_kernel<128, 4>), dim3(total), dim3(kThreads), 0, st, s);
   else
-    hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3(total), dim3(kThreads), 0, st, s);
+    hipLaunchKernelGGL((fwd_bf16_kernel<64, 4>), dim3(total), dim3(kThreads), 0, st, s);
   return hipGetLastError();
 }
 

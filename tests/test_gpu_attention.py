@@ -95,6 +95,60 @@ def test_bf16_forward_invariant_to_block_order():
         assert max_err(lse, lse_ref) <= TOL_O
 
 
+@pytest.mark.parametrize("S,N,causal,full", [(16384, 1, 1, True), (32768, 2, 1, False), (32768, 2, 0, False)])
+def test_bf16_forward_long_blocks(S, N, causal, full):
+    """Blocks of 16384 keys or more run the eight-wave kernel (256 queries per workgroup):
+    a whole head in full on one case (diagonal tiles of every workgroup), otherwise one
+    sampled row of every 32-row wave tile of both heads plus the block edges."""
+    B, H, D = 1, 2, 128
+    q, k, v = synth.attention_inputs(13, B, S, H, D)
+    o, lse = ra.attention_fwd(*dev(q, k, v), N, causal)
+    torch.cuda.synchronize()
+    o, lse = o.cpu(), lse.cpu()
+    c = S // N
+    worst = [0.0, 0.0]
+    for h in range(H):
+        hs = slice(h, h + 1)
+        if full and h == 0:
+            o_ref, lse_ref = OA.attention_fwd(np64(q[:, :, hs]), np64(k[:, :, hs]), np64(v[:, :, hs]), bool(causal))
+            worst[0] = max(worst[0], max_err(o[:, :, hs], o_ref))
+            worst[1] = max(worst[1], max_err(lse[:, hs], lse_ref))
+            continue
+        rng = np.random.default_rng(300 + h)
+        rows = np.arange(0, S, 32) + rng.integers(0, 32, size=S // 32)
+        rows = np.array(sorted(r for r in set(rows.tolist()) | {0, 255, 256, c - 1, c, S - 1} if r < S))
+        o_ref, lse_ref = OA.attention_rows(q[:, :, hs], k[:, :, hs], v[:, :, hs], rows, bool(causal))
+        worst[0] = max(worst[0], max_err(o[:, rows, hs], o_ref))
+        worst[1] = max(worst[1], max_err(lse[:, hs][:, :, rows], lse_ref))
+    log("  S=%d N=%d causal=%d: o %.3e lse %.3e" % (S, N, causal, worst[0], worst[1]))
+    assert worst[0] <= TOL_O and worst[1] <= TOL_O
+
+
+def test_bf16_one_host_share_long_block():
+    """One host's share with 16384-key blocks (eight-wave kernel, side-stream copies into
+    the receive slots): host 1 of 2, sampled rows of both heads."""
+    B, H, D, N, host = 1, 2, 128, 2, 1
+    S = 32768
+    c = S // N
+    q, k, v = synth.attention_inputs(14, B, S, H, D)
+    qb = q[:, host * c:(host + 1) * c].contiguous()
+    o = torch.empty(qb.shape, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((B, H, c), dtype=torch.float32, device="cuda")
+    ra.ring_attn_fwd_host(dev(qb), *dev(k, v), o, lse, N, host, True)
+    torch.cuda.synchronize()
+    o, lse = o.cpu(), lse.cpu()
+    rng = np.random.default_rng(400)
+    rows = np.array(sorted(set((np.arange(0, c, 32) + rng.integers(0, 32, size=c // 32)).tolist()) | {0, c - 1}))
+    worst = [0.0, 0.0]
+    for h in range(H):
+        hs = slice(h, h + 1)
+        o_ref, lse_ref = OA.attention_rows(q[:, :, hs], k[:, :, hs], v[:, :, hs], rows + host * c, True)
+        worst[0] = max(worst[0], max_err(o[:, rows, hs], o_ref))
+        worst[1] = max(worst[1], max_err(lse[:, hs][:, :, rows], lse_ref))
+    log("  host share c=%d: o %.3e lse %.3e" % (c, worst[0], worst[1]))
+    assert worst[0] <= TOL_O and worst[1] <= TOL_O
+
+
 @pytest.mark.parametrize("host", [0, 3, 7])
 def test_bf16_one_host_share(host):
     B, H, D, N, c = 1, 2, 128, 8, 256
