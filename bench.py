@@ -12,7 +12,7 @@ the timed region.  Prints ONE JSON line.
 `value` is TFLOP/s of algorithmic work (4*B*H*D per visible (query, key) pair; causal
 masking halves the diagonal blocks and skips blocks above the diagonal).  The
 `roofline` object reports the step kernel's own throughput (HIP events around every
-launch, on the stream it runs on) against the bf16 dense matrix-core peak, and beside it
+launch, on the stream it runs on, in a second pass of as many calls after the timed ones) against the bf16 dense matrix-core peak, and beside it
 against the rates the chip sustains on back-to-back matrix products alone (the library's
 calibration kernel, measured in the same run): with fixed operands, and with random
 operands that change from product to product as real data does.  `ms_per_step` is the mean over the timed
@@ -361,9 +361,15 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # the timed calls run without the library's per-launch timing events (each leaves the
+    # GPU idle for a few microseconds between two step kernels); the step kernel's own
+    # duration for the roofline is measured in a second pass of as many calls with them
+    ms, ms_med, ms_min, wall = time_calls_each(step, args.steps)
     ra.timing_read(ra.KERNEL_ATTN_FWD)
     ra.timing_enable(True)
-    ms, ms_med, ms_min, wall = time_calls_each(step, args.steps)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
     ra.timing_enable(False)
     kms, launches = ra.timing_read(ra.KERNEL_ATTN_FWD)
     k_avg_ms = kms / max(1, launches)
