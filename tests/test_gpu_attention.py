@@ -95,12 +95,13 @@ def test_bf16_forward_invariant_to_block_order():
         assert max_err(lse, lse_ref) <= TOL_O
 
 
-@pytest.mark.parametrize("S,N,causal,full", [(16384, 1, 1, True), (32768, 2, 1, False), (32768, 2, 0, False)])
-def test_bf16_forward_long_blocks(S, N, causal, full):
+@pytest.mark.parametrize("S,N,causal,full,B", [(16384, 1, 1, True, 1), (32768, 2, 1, False, 1),
+                                               (32768, 2, 0, False, 1), (32768, 2, 1, False, 2)])
+def test_bf16_forward_long_blocks(S, N, causal, full, B):
     """Blocks of 16384 keys or more run the eight-wave kernel (256 queries per workgroup):
     a whole head in full on one case (diagonal tiles of every workgroup), otherwise one
-    sampled row of every 32-row wave tile of both heads plus the block edges."""
-    B, H, D = 1, 2, 128
+    sampled row of every 32-row wave tile of both heads (of every batch) plus the block edges."""
+    H, D = 2, 128
     q, k, v = synth.attention_inputs(13, B, S, H, D)
     o, lse = ra.attention_fwd(*dev(q, k, v), N, causal)
     torch.cuda.synchronize()
