@@ -41,8 +41,10 @@ rounded (the exact values the GPU sees), then upcast.
 Parity status: attention forward/backward, ring bookkeeping, ring decode, FFN and the overlap
 condition (against the paper's printed table, tests/golden/) are pinned by the
 tests in tests/test_oracle_*.py (closed forms, invariants, brute force, finite
-differences, library routines).  The layer composition is pinned only to the
-composition defined in ``layer`` (the paper does not fix norms, biases or the
-activation of that layer), and likewise the composition in ``llama``: for them, parity
-unpinned beyond their parts (each part is pinned).
+differences, library routines).  The two layer compositions (``layer``: the paper fixes
+neither norms, biases nor the activation of that layer; ``llama``: the LLaMA architecture
+around the attention) are readings of the paper: the code is pinned to each reading by a
+restatement in torch library routines with autograd for every gradient and by finite
+differences, ``layer`` also by the closed form of zero query and key weights, and each of
+their parts has its own pins.
 """

@@ -12,9 +12,11 @@ reading and the library follows the same one:
   Z = Y + FFN(Y),  FFN(y) = GeLU_erf(y W1) W2   (no biases)
 
 X has shape [S, d_model] (batch 1).  The backward pass returns the gradients of
-sum(dZ * Z) with respect to X and every weight.  Parity of this composition is pinned
-only to the composition written here (parity unpinned beyond its attention and FFN
-parts, which have their own pins).
+sum(dZ * Z) with respect to X and every weight.  The composition is a reading of the
+paper; the code is pinned to it by a restatement in torch library routines (scaled
+dot-product attention, GeLU, autograd for the gradients), by the closed form that zero
+query and key weights give (causal attention becomes the running mean of the value rows),
+and by central finite differences; its attention and FFN parts have their own pins.
 """
 import numpy as np
 

@@ -18,8 +18,11 @@ this module writes them out from their usual definitions, in float64:
 The attention is the plain definition of ``oracle.attention`` (which the ring result
 equals exactly).  Backward passes follow the chain rule, recomputing nothing that the
 forward returns.  The composition (norm placement, eps, RoPE pairing and base) is a
-reading, not fixed by the paper: parity unpinned beyond the pieces, each of which is pinned
-to a library routine or to a property it must satisfy (tests/test_oracle_llama.py).
+reading, not fixed by the paper; the code is pinned to that reading by a restatement in
+torch library routines (rms_norm, torch.polar rotary embedding, scaled dot-product
+attention, silu) with autograd for every gradient, of the layer and of a two-layer stack,
+and by finite differences; each piece is pinned to a library routine or to a property it
+must satisfy (tests/test_oracle_llama.py).
 """
 import numpy as np
 

@@ -136,3 +136,28 @@ def test_layer_backward_finite_differences():
             am[idx][pos] -= eps
             num[pos] = (loss(ap) - loss(am)) / (2 * eps)
         np.testing.assert_allclose(grads[idx], num, atol=1e-7)
+
+
+def test_layer_uniform_attention_closed_form():
+    """With Wq = Wk = 0 every score is 0, so causal attention is the running mean of the
+    value rows: A = P (X Wv) with P the lower-triangular averaging matrix, and the layer
+    is Z = Y + GeLU(Y W1) W2 with Y = X + A Wo, written here with numpy and scipy's erf
+    alone (no oracle code)."""
+    from scipy.special import erf
+    S, dm, H, dff = 24, 16, 4, 20
+    x = _rand(50, S, dm)
+    wv, wo, w1, w2 = (_rand(51 + i, *shape, std=0.4) for i, shape in
+                      enumerate([(dm, dm), (dm, dm), (dm, dff), (dff, dm)]))
+    zero = np.zeros((dm, dm))
+    z = L.layer_fwd(x, zero, zero, wv, wo, w1, w2, n_heads=H)
+    P = np.tril(np.ones((S, S))) / np.arange(1, S + 1)[:, None]
+    y = x + (P @ (x @ wv)) @ wo
+    h = y @ w1
+    np.testing.assert_allclose(z, y + (0.5 * h * (1.0 + erf(h / np.sqrt(2.0)))) @ w2, atol=1e-12)
+    # without causal masking the mean runs over every row
+    z_full = L.layer_fwd(x, zero, zero, wv, wo, w1, w2, n_heads=H, causal=False)
+    y_full = x + np.mean(x @ wv, axis=0, keepdims=True) @ wo
+    h_full = y_full @ w1
+    np.testing.assert_allclose(z_full, y_full + (0.5 * h_full * (1.0 + erf(h_full / np.sqrt(2.0)))) @ w2,
+                               atol=1e-12)
+

@@ -174,3 +174,20 @@ def test_llama_post_norm_residual_is_caught(monkeypatch):
     import tests.test_oracle_llama as TL
     monkeypatch.setattr(LL, "layer_fwd", _mutated(LL, "layer_fwd", "h = x + a @", "h = n1 + a @"))
     _fails(TL.test_layer_matches_torch_composition, True)
+
+
+def test_layer_ffn_on_the_wrong_input_is_caught(monkeypatch):
+    """The feed-forward network applied to the layer input X instead of Y = X + A Wo."""
+    from oracle import layer as L
+    monkeypatch.setattr(L, "layer_fwd", _mutated(L, "layer_fwd", "_ffn.ffn_fwd(y,", "_ffn.ffn_fwd(x,"))
+    _fails(TF.test_layer_uniform_attention_closed_form)
+    _fails(TF.test_layer_matches_torch_composition)
+
+
+def test_layer_dropped_attention_residual_is_caught(monkeypatch):
+    """Y = A Wo without the residual X."""
+    from oracle import layer as L
+    monkeypatch.setattr(L, "layer_fwd", _mutated(L, "layer_fwd", "y = x + a.reshape", "y = 0 * x + a.reshape"))
+    _fails(TF.test_layer_uniform_attention_closed_form)
+    _fails(TF.test_layer_matches_torch_composition)
+
