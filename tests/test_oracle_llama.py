@@ -183,3 +183,25 @@ def test_stack_matches_torch_composition():
     for li in range(2):
         for g, t in zip(grads[li], tl[li]):
             np.testing.assert_allclose(g, t.grad.numpy(), atol=1e-11)
+
+
+def test_layer_zero_query_key_closed_form():
+    """With zero query and key weights every score is 0 (rotary embedding of zero is zero),
+    so causal attention is the running mean of the value rows; the layer is then written
+    out with numpy alone: n1 = x g1 / rms(x), h = x + P (n1 Wv) Wo with P the lower-triangular
+    averaging matrix, z = h + (silu(n2 W1) * (n2 W3)) W2 with n2 = h g2 / rms(h)."""
+    S, d, H, dff = 24, 16, 4, 20
+    x = _rand(70, S, d)
+    g1, g2 = 1.0 + 0.1 * _rand(71, d), 1.0 + 0.1 * _rand(72, d)
+    wv, wo = _rand(73, d, d, scale=0.4), _rand(74, d, d, scale=0.4)
+    w1, w3, w2 = _rand(75, d, dff, scale=0.4), _rand(76, d, dff, scale=0.4), _rand(77, dff, d, scale=0.4)
+    zero = np.zeros((d, d))
+    z = L.layer_fwd(x, g1, zero, zero, wv, wo, g2, w1, w3, w2, H)
+    rms = lambda t: np.sqrt((t * t).mean(axis=1, keepdims=True) + L.EPS)
+    n1 = x / rms(x) * g1
+    P = np.tril(np.ones((S, S))) / np.arange(1, S + 1)[:, None]
+    h = x + (P @ (n1 @ wv)) @ wo
+    n2 = h / rms(h) * g2
+    u = n2 @ w1
+    np.testing.assert_allclose(z, h + ((u / (1.0 + np.exp(-u))) * (n2 @ w3)) @ w2, atol=1e-12)
+

@@ -174,6 +174,16 @@ def test_llama_post_norm_residual_is_caught(monkeypatch):
     import tests.test_oracle_llama as TL
     monkeypatch.setattr(LL, "layer_fwd", _mutated(LL, "layer_fwd", "h = x + a @", "h = n1 + a @"))
     _fails(TL.test_layer_matches_torch_composition, True)
+    _fails(TL.test_layer_zero_query_key_closed_form)
+
+
+def test_llama_second_norm_on_the_input_is_caught(monkeypatch):
+    """The feed-forward branch normalising x instead of h."""
+    from oracle import llama as LL
+    import tests.test_oracle_llama as TL
+    monkeypatch.setattr(LL, "layer_fwd", _mutated(LL, "layer_fwd", "n2, _ = rmsnorm_fwd(h,", "n2, _ = rmsnorm_fwd(x,"))
+    _fails(TL.test_layer_zero_query_key_closed_form)
+    _fails(TL.test_layer_matches_torch_composition, True)
 
 
 def test_layer_ffn_on_the_wrong_input_is_caught(monkeypatch):
