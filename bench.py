@@ -141,10 +141,13 @@ def cpu_baseline(B, S, H, D, N):
 
 
 def cpu_baselines_other():
-    """The blockwise ring oracle timed on bounded samples of the other attention
-    configurations: forward + backward at S=16384 (1 of 16 heads), and one host's share
-    (host 7 of 8, c=32768; 1 of 32 heads, its first 2 of 8 ring steps, tiles of 4096),
-    each extrapolated linearly to the whole configuration."""
+    """The oracle timed on the other configurations: the float32 ring configuration whole
+    (S=1024, one head of 64, 4 hosts, forward + backward); forward + backward at S=16384
+    (1 of 16 heads); one host's share (host 7 of 8, c=32768; 1 of 32 heads, its first 2 of 8
+    ring steps, tiles of 4096); and the Algorithm 1 layer at S=65536, d_model 4096 (its
+    forward + backward on 512 rows, scaled linearly in rows for the projections and the
+    feed-forward network, plus its attention flops at the S=16384 sample's rate).  Samples
+    are extrapolated linearly to the whole configuration."""
     import numpy as np
     from oracle import ring as OR
     rng = np.random.default_rng(1)
@@ -170,6 +173,33 @@ def cpu_baselines_other():
                                     "whole_s_extrapolated": round(dt * whole / done, 1),
                                     "cores": _torch_threads(),
                                     "sample": "1 of 32 heads, the first 2 of 8 ring steps (diagonal + one full block)"}
+    S1, N1, D1 = 1024, 4, 64
+    q1, k1, v1, do1 = (rng.standard_normal((1, S1, 1, D1)).astype(np.float32) for _ in range(4))
+    t0 = time.perf_counter()
+    OR.ring_attention_bwd(q1, k1, v1, do1, N1, True)  # forward + backward
+    dt = time.perf_counter() - t0
+    out["fp32_S1024_H1_D64"] = {"tflops": round(4.0 * D1 * causal_pairs(S1) * 3.5 / dt / 1e12, 5),
+                                "sample_s": round(dt, 3), "cores": _torch_threads(),
+                                "sample": "the whole configuration, ring forward + backward"}
+    from oracle import layer as OL
+    S4, Ss, dm, dff, H4 = 65536, 512, 4096, 16384, 32
+    x = rng.standard_normal((Ss, dm))
+    ws = [rng.standard_normal(sh) * 0.02 for sh in [(dm, dm)] * 4 + [(dm, dff), (dff, dm)]]
+    dz = rng.standard_normal((Ss, dm))
+    t0 = time.perf_counter()
+    OL.layer_fwd(x, *ws, n_heads=H4)
+    OL.layer_bwd(x, *ws, dz, n_heads=H4)  # recomputes the forward, as the library does
+    dt_rows = time.perf_counter() - t0
+    del x, ws, dz
+    fatt4 = 4.0 * H4 * D * causal_pairs(S4) * 3.5
+    att_rate = out["fwd_bwd_S16384_H16"]["tflops"] * 1e12
+    whole = dt_rows * S4 / Ss + fatt4 / att_rate
+    flayer = fatt4 + 3 * 24.0 * S4 * dm * dm
+    out["layer_fwd_bwd_S65536_d4096"] = {"tflops": round(flayer / whole / 1e12, 5), "sample_s": round(dt_rows, 2),
+                                         "whole_s_extrapolated": round(whole, 1), "cores": _torch_threads(),
+                                         "sample": "oracle layer forward + backward on 512 rows (projections and "
+                                                   "feed-forward network scaled by rows) + attention at the S=16384 "
+                                                   "sample's rate"}
     return out
 
 
