@@ -1,11 +1,15 @@
-"""Seeded parity sweep of the bf16 ring-attention entry points over shapes the fixed grids
-of the other tests do not reach: rings of 3, 5, 6 and 7 hosts (as well as 2 and 8), odd
-head counts, batch 3, blocks of 128 to 384 keys, both head dims, causal and not.
+"""Seeded parity sweeps over shapes the fixed grids of the other tests do not reach.
 
-Each case runs the whole-ring forward and backward and one host's share (its forward, then
-its backward contributions added on top of nonzero carried dK/dV), and compares every
-element with the fp64 oracle on the same inputs.  Tolerances as in the other attention
-tests: 2e-2 on o and lse, 5e-2 on dq, dk, dv (absolute).
+Attention: rings of 3, 5, 6 and 7 hosts (as well as 2 and 8), odd head counts, batch 3,
+blocks of 128 to 384 keys, both head dims, causal and not.  Each case runs the whole-ring
+forward and backward and one host's share (its forward, then its backward contributions
+added on top of nonzero carried dK/dV), and compares every element with the fp64 oracle
+on the same inputs; tolerances as in the other attention tests: 2e-2 on o and lse, 5e-2
+on dq, dk, dv (absolute).
+
+Blockwise FFN: widths that are multiples of 256 but not powers of two, blocks of 256 to
+768 rows, every activation, with and without biases, forward and backward; tolerances as
+in the other FFN tests (magnitude-scaled 2e-2 / 5e-2, weight gradients 5e-2 of their rms).
 """
 import numpy as np
 import pytest
@@ -14,6 +18,7 @@ import torch
 import paper_2310_01889_amd as ra
 from paper_2310_01889_amd import synth
 from oracle import attention as OA
+from oracle import ffn as OF
 from tests.gpu_util import dev, log, max_err, np64
 
 pytestmark = pytest.mark.gpu
@@ -75,3 +80,49 @@ def test_ring_and_host_share_sweep(seed, B, S, H, D, N, causal, host):
     eg = [max_err(dqb, hq), max_err(dk_acc.cpu() - carried_k, hk), max_err(dv_acc.cpu() - carried_v, hv)]
     log("  host %d: o %.3e lse %.3e dq/dk/dv %s" % (host, eo, el, ["%.3e" % x for x in eg]))
     assert eo <= TOL_O and el <= TOL_O and max(eg) <= TOL_G
+
+
+def _ffn_cases():
+    rng = np.random.default_rng(1889)
+    out = []
+    for i in range(10):
+        blk = 256 * int(rng.integers(1, 4))
+        T = blk * int(rng.integers(1, 4))
+        dm = 256 * int(rng.choice([1, 2, 3, 5]))
+        dff = 256 * int(rng.choice([1, 2, 4, 7]))
+        act = int(rng.choice([ra.ACT_GELU_ERF, ra.ACT_RELU, ra.ACT_GELU_TANH]))
+        bias = bool(rng.integers(0, 2))
+        out.append(pytest.param(i, T, dm, dff, blk, act, bias,
+                                id="f%d-T%dd%dff%db%d-a%d-%s" % (i, T, dm, dff, blk, act, "bias" if bias else "nobias")))
+    return out
+
+
+def _scaled_err(got, ref):
+    return float(np.max(np.abs(np64(got) - ref) / np.maximum(1.0, np.abs(ref))))
+
+
+def _wgrad_err(got, ref):
+    return float(np.abs(np64(got) - ref).max()) / max(1.0, float(np.sqrt(np.mean(ref * ref))))
+
+
+@pytest.mark.parametrize("seed,T,dm,dff,blk,act,bias", _ffn_cases())
+def test_blockwise_ffn_sweep(seed, T, dm, dff, blk, act, bias):
+    log("ffn sweep case seed=%d T=%d d_model=%d d_ff=%d block=%d act=%d bias=%d" % (seed, T, dm, dff, blk, act, bias))
+    x, w1, b1, w2, b2, dy = synth.ffn_inputs(700 + seed, T, dm, dff, with_bias=bias, with_grad=True)
+    xd, w1d, w2d, dyd = dev(x, w1, w2, dy)
+    b1d, b2d = (dev(b1), dev(b2)) if bias else (None, None)
+    y = torch.empty((T, dm), dtype=torch.bfloat16, device="cuda")
+    ra.blockwise_ffn(xd, w1d, b1d, w2d, b2d, y, blk, act)
+    dx = torch.empty_like(xd)
+    f32 = lambda *shape: torch.empty(*shape, dtype=torch.float32, device="cuda")
+    dw1, db1, dw2, db2 = f32(dm, dff), f32(dff), f32(dff, dm), f32(dm)
+    ra.blockwise_ffn_bwd(xd, w1d, b1d, w2d, dyd, dx, dw1, db1, dw2, db2, blk, act)
+    torch.cuda.synchronize()
+    x64, w164, w264, dy64 = np64(x), np64(w1), np64(w2), np64(dy)
+    b164, b264 = (np64(b1), np64(b2)) if bias else (None, None)
+    ey = _scaled_err(y, OF.ffn_fwd(x64, w164, b164, w264, b264, act))
+    rdx, rdw1, rdb1, rdw2, rdb2 = OF.ffn_bwd(x64, w164, b164, w264, dy64, act)
+    edx = _scaled_err(dx, rdx)
+    ew = [_wgrad_err(g, r) for g, r in ((dw1, rdw1), (db1, rdb1), (dw2, rdw2), (db2, rdb2))]
+    log("  y %.3e dx %.3e dw1/db1/dw2/db2 (of rms) %s" % (ey, edx, ["%.3e" % e for e in ew]))
+    assert ey <= 2e-2 and edx <= 5e-2 and max(ew) <= 5e-2
