@@ -7,6 +7,10 @@ added on top of nonzero carried dK/dV), and compares every element with the fp64
 on the same inputs; tolerances as in the other attention tests: 2e-2 on o and lse, 5e-2
 on dq, dk, dv (absolute).
 
+Ring decode: rings of 1 to 8 hosts (mostly odd), cache blocks of 32 to 640 keys, batch up
+to 3, odd head counts, 1 to 32 queries, both head dims and masks; o and lse against the
+oracle's ring decode, 2e-2 absolute.
+
 Blockwise FFN: widths that are multiples of 256 but not powers of two, blocks of 256 to
 768 rows, every activation, with and without biases, forward and backward; tolerances as
 in the other FFN tests (magnitude-scaled 2e-2 / 5e-2, weight gradients 5e-2 of their rms).
@@ -18,6 +22,7 @@ import torch
 import paper_2310_01889_amd as ra
 from paper_2310_01889_amd import synth
 from oracle import attention as OA
+from oracle import decode as OD
 from oracle import ffn as OF
 from tests.gpu_util import dev, log, max_err, np64
 
@@ -126,3 +131,31 @@ def test_blockwise_ffn_sweep(seed, T, dm, dff, blk, act, bias):
     ew = [_wgrad_err(g, r) for g, r in ((dw1, rdw1), (db1, rdb1), (dw2, rdw2), (db2, rdb2))]
     log("  y %.3e dx %.3e dw1/db1/dw2/db2 (of rms) %s" % (ey, edx, ["%.3e" % e for e in ew]))
     assert ey <= 2e-2 and edx <= 5e-2 and max(ew) <= 5e-2
+
+
+def _decode_cases():
+    rng = np.random.default_rng(2023)
+    out = []
+    for i in range(12):
+        N = int(rng.choice([1, 3, 5, 6, 7, 8]))
+        c = 32 * int(rng.integers(1, 21))
+        B = int(rng.choice([1, 2, 3]))
+        H = int(rng.choice([1, 3, 5]))
+        D = int(rng.choice([64, 128]))
+        Tq = int(rng.integers(1, min(32, N * c) + 1))
+        causal = int(rng.integers(0, 2))
+        out.append(pytest.param(i, B, N * c, H, D, Tq, N, causal,
+                                id="d%d-B%dS%dH%dD%dTq%dN%d-c%d" % (i, B, N * c, H, D, Tq, N, causal)))
+    return out
+
+
+@pytest.mark.parametrize("seed,B,S,H,D,Tq,N,causal", _decode_cases())
+def test_ring_decode_sweep(seed, B, S, H, D, Tq, N, causal):
+    log("decode sweep case seed=%d B=%d S=%d H=%d D=%d Tq=%d N=%d causal=%d" % (seed, B, S, H, D, Tq, N, causal))
+    q, k, v = synth.attention_inputs(900 + seed, B, Tq, H, D, kv_len=S)
+    o, lse = ra.attention_decode(*dev(q, k, v), N, causal)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = OD.ring_decode_fwd(np64(q), np64(k), np64(v), N, bool(causal))
+    eo, el = max_err(o, o_ref), max_err(lse, lse_ref)
+    log("  o %.3e lse %.3e" % (eo, el))
+    assert eo <= TOL_O and el <= TOL_O
