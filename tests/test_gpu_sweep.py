@@ -11,6 +11,10 @@ Ring decode: rings of 1 to 8 hosts (mostly odd), cache blocks of 32 to 640 keys,
 to 3, odd head counts, 1 to 32 queries, both head dims and masks; o and lse against the
 oracle's ring decode, 2e-2 absolute.
 
+Algorithm 1 layer: rings of 3, 5 and 6 hosts with blocks of 256 rows, d_model 256-768
+split into 2-12 heads of 64 or 128, d_ff 512-1024; z and dx magnitude-scaled (2e-2 / 5e-2)
+and the weight gradients as the other layer tests bound them.
+
 Blockwise FFN: widths that are multiples of 256 but not powers of two, blocks of 256 to
 768 rows, every activation, with and without biases, forward and backward; tolerances as
 in the other FFN tests (magnitude-scaled 2e-2 / 5e-2, weight gradients 5e-2 of their rms).
@@ -24,6 +28,7 @@ from paper_2310_01889_amd import synth
 from oracle import attention as OA
 from oracle import decode as OD
 from oracle import ffn as OF
+from oracle import layer as OL
 from tests.gpu_util import dev, log, max_err, np64
 
 pytestmark = pytest.mark.gpu
@@ -159,3 +164,28 @@ def test_ring_decode_sweep(seed, B, S, H, D, Tq, N, causal):
     eo, el = max_err(o, o_ref), max_err(lse, lse_ref)
     log("  o %.3e lse %.3e" % (eo, el))
     assert eo <= TOL_O and el <= TOL_O
+
+
+_LAYER_CASES = [  # (seed, n_hosts, d_model, heads, d_ff)
+    (0, 3, 256, 4, 512),
+    (1, 5, 512, 4, 768),
+    (2, 6, 768, 12, 512),
+    (3, 3, 768, 6, 1024),
+]
+
+
+@pytest.mark.parametrize("seed,N,dm,H,dff", _LAYER_CASES,
+                         ids=["l%d-N%dd%dH%dff%d" % c for c in _LAYER_CASES])
+def test_layer_sweep(seed, N, dm, H, dff):
+    from tests.test_gpu_layer import _run_layer, _scaled_err as _layer_err, _wgrad_ok
+    S = 256 * N
+    log("layer sweep case seed=%d S=%d n_hosts=%d d_model=%d heads=%d d_ff=%d" % (seed, S, N, dm, H, dff))
+    ins, z, grads = _run_layer(1000 + seed, S, dm, H, dff, N)
+    x, wq, wk, wv, wo, w1, w2, dz = (np64(t) for t in ins)
+    ez = _layer_err(z, OL.layer_fwd(x, wq, wk, wv, wo, w1, w2, H))
+    ref = OL.layer_bwd(x, wq, wk, wv, wo, w1, w2, dz, H)
+    edx = _layer_err(grads[0], ref[0])
+    log("  z %.3e dx %.3e (scaled)" % (ez, edx))
+    assert ez <= 2e-2 and edx <= 5e-2
+    for g, r in zip(grads[1:], ref[1:]):
+        assert _wgrad_ok(g, r)
