@@ -18,31 +18,48 @@ namespace {
 
 
 // -------------------------------------------------------------------------------------
-// Delta_r = sum_d dO_rd * O_rd  (float32 [B, H, S]); rows in memory order (b, r, h).
+// Delta_r = sum_d dO_rd * O_rd  (float32 [B, H, S]).  A workgroup takes kPreRows
+// consecutive query rows of one (batch, head): TPR threads per row read that row of o and
+// dO (rows in memory order (b, r, h)), the row sums pass through LDS, and kPreRows threads
+// then write the workgroup's results (and read lse) as contiguous runs of kPreRows floats.
 // The bf16 step kernels take -Delta and -lse sqrt(D) (their accumulators start there:
 // the score accumulators hold q.k, in units of the unscaled products).
 // -------------------------------------------------------------------------------------
+constexpr int kPreRows = 64;
+
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const bf16* dO, const float* lse,
                                                            float* ndelta, float* nlse_s, int B, int S, int H) {
-  constexpr int TPR = D / 8;  // threads per row
-  const long long row = (long long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+  constexpr int TPR = D / 8;      // threads per row
+  constexpr int RPP = 256 / TPR;  // rows per pass
+  constexpr int NP = kPreRows / RPP;
+  __shared__ float sums[kPreRows];
+  const int nrt = (S + kPreRows - 1) / kPreRows;
+  const int bh = blockIdx.x / nrt, r0 = (blockIdx.x % nrt) * kPreRows;
+  const int b = bh / H, h = bh % H;
   const int c = (threadIdx.x % TPR) * 8;
-  const long long nrows = (long long)B * S * H;
-  float s = 0.f;
-  if (row < nrows) {
-    const bf16x8 a = *(const bf16x8*)(o + row * D + c);
-    const bf16x8 g = *(const bf16x8*)(dO + row * D + c);
-    #pragma unroll
-    for (int e = 0; e < 8; ++e) s = fmaf((float)a[e], (float)g[e], s);
+  float s[NP];
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    const int r = r0 + k * RPP + threadIdx.x / TPR;
+    s[k] = 0.f;
+    if (r < S) {
+      const long long row = ((long long)b * S + r) * H + h;
+      const bf16x8 a = *(const bf16x8*)(o + row * D + c);
+      const bf16x8 g = *(const bf16x8*)(dO + row * D + c);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[k] = fmaf((float)a[e], (float)g[e], s[k]);
+    }
   }
-  for (int off = TPR / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-  if (row < nrows && threadIdx.x % TPR == 0) {
-    const int h = (int)(row % H);
-    const long long br = row / H;
-    const int r = (int)(br % S), b = (int)(br / S);
-    const long long idx = ((long long)b * H + h) * S + r;
-    ndelta[idx] = -s;
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    for (int off = TPR / 2; off > 0; off >>= 1) s[k] += __shfl_xor(s[k], off, 64);
+    if (threadIdx.x % TPR == 0) sums[k * RPP + threadIdx.x / TPR] = s[k];
+  }
+  __syncthreads();
+  if (threadIdx.x < kPreRows && r0 + (int)threadIdx.x < S) {
+    const long long idx = (long long)bh * S + r0 + threadIdx.x;
+    ndelta[idx] = -sums[threadIdx.x];
     nlse_s[idx] = -lse[idx] * sqrtf((float)D);  // lse / scale: units of q.k
   }
 }
@@ -51,23 +68,33 @@ template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const float* dO, float* delta,
                                                           int B, int S, int H) {
   constexpr int TPR = D / 4;
-  const long long row = (long long)blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+  constexpr int RPP = 256 / TPR;
+  constexpr int NP = kPreRows / RPP;
+  __shared__ float sums[kPreRows];
+  const int nrt = (S + kPreRows - 1) / kPreRows;
+  const int bh = blockIdx.x / nrt, r0 = (blockIdx.x % nrt) * kPreRows;
+  const int b = bh / H, h = bh % H;
   const int c = (threadIdx.x % TPR) * 4;
-  const long long nrows = (long long)B * S * H;
-  float s = 0.f;
-  if (row < nrows) {
-    const f32x4 a = *(const f32x4*)(o + row * D + c);
-    const f32x4 g = *(const f32x4*)(dO + row * D + c);
-    #pragma unroll
-    for (int e = 0; e < 4; ++e) s = fmaf(a[e], g[e], s);
+  float s[NP];
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    const int r = r0 + k * RPP + threadIdx.x / TPR;
+    s[k] = 0.f;
+    if (r < S) {
+      const long long row = ((long long)b * S + r) * H + h;
+      const f32x4 a = *(const f32x4*)(o + row * D + c);
+      const f32x4 g = *(const f32x4*)(dO + row * D + c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s[k] = fmaf(a[e], g[e], s[k]);
+    }
   }
-  for (int off = TPR / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-  if (row < nrows && threadIdx.x % TPR == 0) {
-    const int h = (int)(row % H);
-    const long long br = row / H;
-    const int r = (int)(br % S), b = (int)(br / S);
-    delta[((long long)b * H + h) * S + r] = s;
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    for (int off = TPR / 2; off > 0; off >>= 1) s[k] += __shfl_xor(s[k], off, 64);
+    if (threadIdx.x % TPR == 0) sums[k * RPP + threadIdx.x / TPR] = s[k];
   }
+  __syncthreads();
+  if (threadIdx.x < kPreRows && r0 + (int)threadIdx.x < S) delta[(long long)bh * S + r0 + threadIdx.x] = sums[threadIdx.x];
 }
 
 // Adds a workgroup's dK (DK) or dV contribution (lanes over keys, accumulated transposed:
@@ -1215,9 +1242,7 @@ __global__ void zero_f32_kernel(float* p, long long n) {
 
 hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, float* delta, float* nlse_s, int B,
                                int S, int H, int D, hipStream_t st) {
-  const long long rows = (long long)B * S * H;
-  const int rpb = 256 / (D / 8);
-  const long long blocks = (rows + rpb - 1) / rpb;
+  const long long blocks = (long long)B * H * ((S + kPreRows - 1) / kPreRows);
   if (D == 128)
     hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, nlse_s, B, S, H);
   else
@@ -1227,9 +1252,7 @@ hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, 
 
 hipError_t launch_bwd_pre_f32(const float* o, const float* dO, float* delta, int B, int S, int H, int D,
                               hipStream_t st) {
-  const long long rows = (long long)B * S * H;
-  const int rpb = 256 / (D / 4);
-  const long long blocks = (rows + rpb - 1) / rpb;
+  const long long blocks = (long long)B * H * ((S + kPreRows - 1) / kPreRows);
   if (D == 128)
     hipLaunchKernelGGL(bwd_pre_f32_kernel<128>, dim3(blocks), dim3(256), 0, st, o, dO, delta, B, S, H);
   else
