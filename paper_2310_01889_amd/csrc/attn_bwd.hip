@@ -18,32 +18,40 @@ namespace {
 
 
 // -------------------------------------------------------------------------------------
-// Delta_r = sum_d dO_rd * O_rd  (float32 [B, H, S]).  A workgroup takes kPreRows
-// consecutive query rows of one (batch, head): TPR threads per row read that row of o and
-// dO (rows in memory order (b, r, h)), the row sums pass through LDS, and kPreRows threads
-// then write the workgroup's results (and read lse) as contiguous runs of kPreRows floats.
+// Delta_r = sum_d dO_rd * O_rd  (float32 [B, H, S]).  A workgroup takes a tile of kPreR
+// consecutive query rows x kPreH consecutive heads of one batch: TPR threads per (row,
+// head) read that row of o and dO, heads fastest (so a row's kPreH heads are one contiguous
+// run of memory); the sums pass through LDS, and the results (and lse) are then written
+// (read) head by head as runs of kPreR consecutive floats.
 // The bf16 step kernels take -Delta and -lse sqrt(D) (their accumulators start there:
 // the score accumulators hold q.k, in units of the unscaled products).
 // -------------------------------------------------------------------------------------
-constexpr int kPreRows = 64;
+constexpr int kPreR = 16, kPreH = 8, kPreTile = kPreR * kPreH;
+
+__device__ __forceinline__ void pre_tile(int S, int H, int& b, int& r0, int& h0) {
+  const int nht = (H + kPreH - 1) / kPreH, nrt = (S + kPreR - 1) / kPreR;
+  const int t = blockIdx.x;
+  h0 = (t % nht) * kPreH;
+  r0 = ((t / nht) % nrt) * kPreR;
+  b = t / (nht * nrt);
+}
 
 template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const bf16* dO, const float* lse,
                                                            float* ndelta, float* nlse_s, int B, int S, int H) {
-  constexpr int TPR = D / 8;      // threads per row
-  constexpr int RPP = 256 / TPR;  // rows per pass
-  constexpr int NP = kPreRows / RPP;
-  __shared__ float sums[kPreRows];
-  const int nrt = (S + kPreRows - 1) / kPreRows;
-  const int bh = blockIdx.x / nrt, r0 = (blockIdx.x % nrt) * kPreRows;
-  const int b = bh / H, h = bh % H;
+  constexpr int TPR = D / 8;      // threads per (row, head)
+  constexpr int RPP = 256 / TPR;  // (row, head) pairs per pass
+  constexpr int NP = kPreTile / RPP;
+  __shared__ float sums[kPreTile];
+  int b, r0, h0;
+  pre_tile(S, H, b, r0, h0);
   const int c = (threadIdx.x % TPR) * 8;
   float s[NP];
 #pragma unroll
   for (int k = 0; k < NP; ++k) {
-    const int r = r0 + k * RPP + threadIdx.x / TPR;
+    const int q = k * RPP + threadIdx.x / TPR, r = r0 + q / kPreH, h = h0 + q % kPreH;
     s[k] = 0.f;
-    if (r < S) {
+    if (r < S && h < H) {
       const long long row = ((long long)b * S + r) * H + h;
       const bf16x8 a = *(const bf16x8*)(o + row * D + c);
       const bf16x8 g = *(const bf16x8*)(dO + row * D + c);
@@ -57,10 +65,13 @@ __global__ __launch_bounds__(256) void bwd_pre_bf16_kernel(const bf16* o, const 
     if (threadIdx.x % TPR == 0) sums[k * RPP + threadIdx.x / TPR] = s[k];
   }
   __syncthreads();
-  if (threadIdx.x < kPreRows && r0 + (int)threadIdx.x < S) {
-    const long long idx = (long long)bh * S + r0 + threadIdx.x;
-    ndelta[idx] = -sums[threadIdx.x];
-    nlse_s[idx] = -lse[idx] * sqrtf((float)D);  // lse / scale: units of q.k
+  if (threadIdx.x < kPreTile) {
+    const int r = r0 + threadIdx.x % kPreR, h = h0 + threadIdx.x / kPreR;
+    if (r < S && h < H) {
+      const long long idx = ((long long)b * H + h) * S + r;
+      ndelta[idx] = -sums[(threadIdx.x % kPreR) * kPreH + threadIdx.x / kPreR];
+      nlse_s[idx] = -lse[idx] * sqrtf((float)D);  // lse / scale: units of q.k
+    }
   }
 }
 
@@ -69,18 +80,17 @@ __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const 
                                                           int B, int S, int H) {
   constexpr int TPR = D / 4;
   constexpr int RPP = 256 / TPR;
-  constexpr int NP = kPreRows / RPP;
-  __shared__ float sums[kPreRows];
-  const int nrt = (S + kPreRows - 1) / kPreRows;
-  const int bh = blockIdx.x / nrt, r0 = (blockIdx.x % nrt) * kPreRows;
-  const int b = bh / H, h = bh % H;
+  constexpr int NP = kPreTile / RPP;
+  __shared__ float sums[kPreTile];
+  int b, r0, h0;
+  pre_tile(S, H, b, r0, h0);
   const int c = (threadIdx.x % TPR) * 4;
   float s[NP];
 #pragma unroll
   for (int k = 0; k < NP; ++k) {
-    const int r = r0 + k * RPP + threadIdx.x / TPR;
+    const int q = k * RPP + threadIdx.x / TPR, r = r0 + q / kPreH, h = h0 + q % kPreH;
     s[k] = 0.f;
-    if (r < S) {
+    if (r < S && h < H) {
       const long long row = ((long long)b * S + r) * H + h;
       const f32x4 a = *(const f32x4*)(o + row * D + c);
       const f32x4 g = *(const f32x4*)(dO + row * D + c);
@@ -94,7 +104,10 @@ __global__ __launch_bounds__(256) void bwd_pre_f32_kernel(const float* o, const 
     if (threadIdx.x % TPR == 0) sums[k * RPP + threadIdx.x / TPR] = s[k];
   }
   __syncthreads();
-  if (threadIdx.x < kPreRows && r0 + (int)threadIdx.x < S) delta[(long long)bh * S + r0 + threadIdx.x] = sums[threadIdx.x];
+  if (threadIdx.x < kPreTile) {
+    const int r = r0 + threadIdx.x % kPreR, h = h0 + threadIdx.x / kPreR;
+    if (r < S && h < H) delta[((long long)b * H + h) * S + r] = sums[(threadIdx.x % kPreR) * kPreH + threadIdx.x / kPreR];
+  }
 }
 
 // Adds a workgroup's dK (DK) or dV contribution (lanes over keys, accumulated transposed:
@@ -1242,7 +1255,7 @@ __global__ void zero_f32_kernel(float* p, long long n) {
 
 hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, float* delta, float* nlse_s, int B,
                                int S, int H, int D, hipStream_t st) {
-  const long long blocks = (long long)B * H * ((S + kPreRows - 1) / kPreRows);
+  const long long blocks = (long long)B * ((S + kPreR - 1) / kPreR) * ((H + kPreH - 1) / kPreH);
   if (D == 128)
     hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, dim3(blocks), dim3(256), 0, st, (const bf16*)o, (const bf16*)dO, lse, delta, nlse_s, B, S, H);
   else
@@ -1252,7 +1265,7 @@ hipError_t launch_bwd_pre_bf16(const void* o, const void* dO, const float* lse, 
 
 hipError_t launch_bwd_pre_f32(const float* o, const float* dO, float* delta, int B, int S, int H, int D,
                               hipStream_t st) {
-  const long long blocks = (long long)B * H * ((S + kPreRows - 1) / kPreRows);
+  const long long blocks = (long long)B * ((S + kPreR - 1) / kPreR) * ((H + kPreH - 1) / kPreH);
   if (D == 128)
     hipLaunchKernelGGL(bwd_pre_f32_kernel<128>, dim3(blocks), dim3(256), 0, st, o, dO, delta, B, S, H);
   else
