@@ -26,6 +26,8 @@
  *   - Tensors are dense row-major.  q, k, v, o, dO, dq, dk, dv: [B, S, H, D] (batch,
  *     position, head, dim per head; the layout of the paper's code).  lse: float32
  *     [B, H, S], holding max + ln(denominator) of the scaled scores (natural log).
+ *   - Every tensor except lse (and the optional per-row rstd of rms_norm_fwd) starts on a
+ *     16-byte boundary; lse and rstd on a 4-byte one.  Other pointers give RA_EINVAL.
  *   - "bf16" tensors hold IEEE bfloat16 (hip_bfloat16 / torch.bfloat16).  Products are
  *     taken in bf16 with float32 accumulation (the paper's float32-logits option);
  *     softmax statistics, accumulators and weight gradients are float32; outputs are

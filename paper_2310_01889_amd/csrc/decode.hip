@@ -310,6 +310,7 @@ using namespace ra;
 static int decode_validate(const void* q, const void* k_cache, const void* v_cache, const void* o, const float* lse,
                            int B, int H, int S, int D, int Tq, int n_hosts, int causal) {
   if (!q || !k_cache || !v_cache || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k_cache, v_cache, o}, {lse})) return e;
   if (B <= 0 || H <= 0 || S <= 0 || D <= 0 || Tq <= 0 || n_hosts <= 0)
     return set_err(RA_EINVAL, "sizes must be positive (B=%d H=%d S=%d D=%d Tq=%d n_hosts=%d)", B, H, S, D, Tq,
                    n_hosts);

@@ -227,6 +227,7 @@ int blockwise_ffn(const void* x, const void* w1, const void* b1, const void* w2,
                   int d_model, int d_ff, int block, int act, hipStream_t stream) {
   g_err.clear();
   if (!x || !w1 || !w2 || !y) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, w1, b1, w2, b2, y})) return e;
   if (act < 0 || act > 2) return set_err(RA_EINVAL, "act=%d is not an ra_act value", act);
   int rc = check_gemm_dims(T, d_model, d_ff, block);
   if (rc) return rc;
@@ -238,6 +239,7 @@ int blockwise_ffn_bwd(const void* x, const void* w1, const void* b1, const void*
                       int act, hipStream_t stream) {
   g_err.clear();
   if (!x || !w1 || !w2 || !dy || !dx || !dw1 || !dw2) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, w1, b1, w2, dy, dx, dw1, db1, dw2, db2})) return e;
   if (act < 0 || act > 2) return set_err(RA_EINVAL, "act=%d is not an ra_act value", act);
   int rc = check_gemm_dims(T, d_model, d_ff, block);
   if (rc) return rc;
@@ -248,6 +250,7 @@ int blockwise_linear(const void* x, const void* w, const void* residual, void* y
                      int block, hipStream_t stream) {
   g_err.clear();
   if (!x || !w || !y) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, w, residual, y})) return e;
   int rc = check_gemm_dims(T, d_in, d_out, block);
   if (rc) return rc;
   for (int r0 = 0; r0 < T; r0 += block) {
@@ -271,6 +274,7 @@ int blockwise_linear_bwd(const void* x, const void* w, const void* dy, void* dx,
                          int d_out, int block, hipStream_t stream) {
   g_err.clear();
   if (!x || !w || !dy || !dw) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, w, dy, dx, dw})) return e;
   int rc = check_gemm_dims(T, d_in, d_out, block);
   if (rc) return rc;
   for (int bi = 0, r0 = 0; r0 < T; ++bi, r0 += block) {

@@ -69,6 +69,7 @@ int ring_layer_fwd(const void* x, const void* wq, const void* wk, const void* wv
                    int act, hipStream_t stream) {
   g_err.clear();
   if (!x || !wq || !wk || !wv || !wo || !w1 || !w2 || !z) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, wq, wk, wv, wo, w1, w2, z})) return e;
   int rc = check_layer(S, d_model, n_heads, d_ff, n_hosts, causal, act);
   if (rc) return rc;
   CallResources R(stream);
@@ -87,6 +88,7 @@ int ring_layer_bwd(const void* x, const void* wq, const void* wk, const void* wv
   g_err.clear();
   if (!x || !wq || !wk || !wv || !wo || !w1 || !w2 || !dz || !dx || !dwq || !dwk || !dwv || !dwo || !dw1 || !dw2)
     return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, wq, wk, wv, wo, w1, w2, dz, dx, dwq, dwk, dwv, dwo, dw1, dw2})) return e;
   int rc = check_layer(S, d_model, n_heads, d_ff, n_hosts, causal, act);
   if (rc) return rc;
   const int c = S / n_hosts, H = n_heads, dm = d_model;

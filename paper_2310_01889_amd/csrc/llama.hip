@@ -478,6 +478,7 @@ extern "C" {
 int rms_norm_fwd(const void* x, const void* g, void* y, float* rstd, int T, int d, hipStream_t stream) {
   g_err.clear();
   if (!x || !g || !y) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, g, y}, {rstd})) return e;
   int rc = check_norm(T, d);
   if (rc) return rc;
   return norm_fwd(x, g, y, rstd, T, d, stream);
@@ -487,6 +488,7 @@ int rms_norm_bwd(const void* x, const void* g, const float* dy, const void* dres
                  hipStream_t stream) {
   g_err.clear();
   if (!x || !g || !dy || !dx || !dg) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, g, dy, dres, dx, dg})) return e;
   int rc = check_norm(T, d);
   if (rc) return rc;
   CallResources R(stream);
@@ -497,6 +499,7 @@ int rms_norm_bwd(const void* x, const void* g, const float* dy, const void* dres
 int rope_apply(void* x, int S, int H, int D, int pos0, int inverse, hipStream_t stream) {
   g_err.clear();
   if (!x) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x})) return e;
   if (S <= 0 || H <= 0 || D <= 0 || pos0 < 0) return set_err(RA_EINVAL, "sizes must be positive, pos0 >= 0");
   if (inverse != 0 && inverse != 1) return set_err(RA_EINVAL, "inverse must be 0 or 1");
   if (D % 4) return set_err(RA_EUNSUPPORTED, "head dim D=%d must be a multiple of 4", D);
@@ -513,6 +516,7 @@ int swiglu_ffn(const void* x, const void* w1, const void* w3, const void* w2, co
                int d_model, int d_ff, int block, hipStream_t stream) {
   g_err.clear();
   if (!x || !w1 || !w3 || !w2 || !y) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, w1, w3, w2, residual, y})) return e;
   int rc = check_gemm_dims(T, d_model, d_ff, block);
   if (rc) return rc;
   return swiglu_forward(x, w1, w3, w2, residual, y, T, d_model, d_ff, block, stream);
@@ -522,6 +526,7 @@ int swiglu_ffn_bwd(const void* x, const void* w1, const void* w3, const void* w2
                    float* dw3, float* dw2, int T, int d_model, int d_ff, int block, hipStream_t stream) {
   g_err.clear();
   if (!x || !w1 || !w3 || !w2 || !dy || !dx || !dw1 || !dw3 || !dw2) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({x, w1, w3, w2, dy, dx, dw1, dw3, dw2})) return e;
   int rc = check_gemm_dims(T, d_model, d_ff, block);
   if (rc) return rc;
   CallResources R(stream);
@@ -538,6 +543,9 @@ int llama_layer_fwd(const void* x, const void* const* params, void* z, int S, in
   if (!x || !params || !z) return set_err(RA_EINVAL, "null pointer argument");
   for (int i = 0; i < 9; ++i)
     if (!params[i]) return set_err(RA_EINVAL, "null parameter pointer %d", i);
+  if (int e = check_aligned({x, z})) return e;
+  for (int i = 0; i < 9; ++i)
+    if (int e = check_aligned({params[i]})) return e;
   int rc = check_llama(S, d_model, n_heads, d_ff, n_hosts, causal);
   if (rc) return rc;
   CallResources R(stream);
@@ -553,6 +561,9 @@ int llama_layer_bwd(const void* x, const void* const* params, const void* dz, vo
   if (!x || !params || !dz || !dx || !grads) return set_err(RA_EINVAL, "null pointer argument");
   for (int i = 0; i < 9; ++i)
     if (!params[i] || !grads[i]) return set_err(RA_EINVAL, "null parameter or gradient pointer %d", i);
+  if (int e = check_aligned({x, dz, dx})) return e;
+  for (int i = 0; i < 9; ++i)
+    if (int e = check_aligned({params[i], grads[i]})) return e;
   int rc = check_llama(S, d_model, n_heads, d_ff, n_hosts, causal);
   if (rc) return rc;
   return llama_backward(x, params, dz, dx, grads, S, d_model, n_heads, d_ff, n_hosts, causal, stream);
@@ -566,6 +577,9 @@ int llama_stack_train_step(const void* x, const void* const* params, const void*
   if (n_layers <= 0) return set_err(RA_EINVAL, "n_layers=%d must be positive", n_layers);
   for (int i = 0; i < 9 * n_layers; ++i)
     if (!params[i] || !grads[i]) return set_err(RA_EINVAL, "null parameter or gradient pointer %d", i);
+  if (int e = check_aligned({x, dz, z, dx})) return e;
+  for (int i = 0; i < 9 * n_layers; ++i)
+    if (int e = check_aligned({params[i], grads[i]})) return e;
   int rc = check_llama(S, d_model, n_heads, d_ff, n_hosts, causal);
   if (rc) return rc;
   const size_t t = (size_t)S * d_model * 2;

@@ -4,6 +4,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
+#include <initializer_list>
 #include <string>
 #include <vector>
 
@@ -21,6 +23,17 @@ int set_err(int code, const char* fmt, ...);
       return set_err(e_ == hipErrorOutOfMemory ? RA_ENOMEM : RA_EHIP, "%s failed: %s", \
                      #expr, hipGetErrorString(e_));                                    \
   } while (0)
+
+// Tensors made of rows of elements are read and written with 16-byte vector accesses from
+// their start, so they must begin on a 16-byte boundary (rows16); float32 per-row vectors
+// such as lse on a 4-byte one (vec4).  A null pointer (an absent optional argument) passes.
+inline int check_aligned(std::initializer_list<const void*> rows16, std::initializer_list<const void*> vec4 = {}) {
+  for (const void* p : rows16)
+    if (reinterpret_cast<uintptr_t>(p) & 15u) return set_err(RA_EINVAL, "tensor pointer %p is not 16-byte aligned", p);
+  for (const void* p : vec4)
+    if (reinterpret_cast<uintptr_t>(p) & 3u) return set_err(RA_EINVAL, "pointer %p is not 4-byte aligned", p);
+  return RA_OK;
+}
 
 // The current device's workspace pool: a stream-ordered memory pool owned by the library
 // (created on first use, release threshold unlimited, so workspace freed at the end of a

@@ -694,6 +694,7 @@ int ring_attn_fwd(const void* q, const void* k, const void* v, void* o, float* l
                   int n_hosts, int causal, hipStream_t stream) {
   g_err.clear();
   if (!q || !k || !v || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k, v, o}, {lse})) return e;
   int rc = validate(B, H, S, D, n_hosts, causal, 128);
   if (rc) return rc;
   return run_fwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 2), o, lse, stream);
@@ -703,6 +704,7 @@ int ring_attn_fwd_f32(const float* q, const float* k, const float* v, float* o, 
                       int D, int n_hosts, int causal, hipStream_t stream) {
   g_err.clear();
   if (!q || !k || !v || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k, v, o}, {lse})) return e;
   int rc = validate(B, H, S, D, n_hosts, causal, 64);
   if (rc) return rc;
   return run_fwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 4), o, lse, stream);
@@ -712,6 +714,7 @@ int ring_attn_fwd_host(const void* q_blk, const void* k_all, const void* v_all, 
                        int H, int S, int D, int n_hosts, int host_idx, int causal, hipStream_t stream) {
   g_err.clear();
   if (!q_blk || !k_all || !v_all || !o_blk || !lse_blk) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q_blk, k_all, v_all, o_blk}, {lse_blk})) return e;
   int rc = validate(B, H, S, D, n_hosts, causal, 128);
   if (rc) return rc;
   if (host_idx < 0 || host_idx >= n_hosts)
@@ -724,6 +727,7 @@ int ring_attn_fwd_ordered(const void* q, const void* k, const void* v, void* o, 
                           int D, int n_hosts, int causal, const int* kv_order, hipStream_t stream) {
   g_err.clear();
   if (!q || !k || !v || !o || !lse || !kv_order) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k, v, o}, {lse, kv_order})) return e;
   int rc = validate(B, H, S, D, n_hosts, causal, 128);
   if (rc) return rc;
   RingProblem P = all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 2);
@@ -745,6 +749,7 @@ int ring_attn_bwd_host(const void* q_blk, const void* k_all, const void* v_all, 
   g_err.clear();
   if (!q_blk || !k_all || !v_all || !o_blk || !lse_blk || !dO_blk || !dq_blk || !dk_acc || !dv_acc)
     return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q_blk, k_all, v_all, o_blk, dO_blk, dq_blk, dk_acc, dv_acc}, {lse_blk})) return e;
   int rc = validate(B, H, S, D, n_hosts, causal, 128);
   if (rc) return rc;
   if (host_idx < 0 || host_idx >= n_hosts)
@@ -758,6 +763,7 @@ int ring_attn_bwd(const void* q, const void* k, const void* v, const void* o, co
                   hipStream_t stream) {
   g_err.clear();
   if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k, v, o, dO, dq, dk, dv}, {lse})) return e;
   int rc = validate(B, H, S, D, n_hosts, causal, 128);
   if (rc) return rc;
   return run_bwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 2), o, lse, dO, dq, dk, dv, stream);
@@ -768,6 +774,7 @@ int ring_attn_bwd_f32(const float* q, const float* k, const float* v, const floa
                       int causal, hipStream_t stream) {
   g_err.clear();
   if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k, v, o, dO, dq, dk, dv}, {lse})) return e;
   int rc = validate(B, H, S, D, n_hosts, causal, 64);
   if (rc) return rc;
   return run_bwd(all_hosts(q, k, v, B, H, S, D, n_hosts, causal, 4), o, lse, dO, dq, dk, dv, stream);
@@ -777,6 +784,7 @@ int ring_attn_fwd_varlen(const void* q, const void* k, const void* v, void* o, f
                          int D, int n_hosts, hipStream_t stream) {
   g_err.clear();
   if (!q || !k || !v || !o || !lse) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k, v, o}, {lse})) return e;
   long long Sp = 0;
   int rc = padded_len(S, n_hosts, &Sp);
   if (rc) return rc;
@@ -802,6 +810,7 @@ int ring_attn_bwd_varlen(const void* q, const void* k, const void* v, const void
                          hipStream_t stream) {
   g_err.clear();
   if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv) return set_err(RA_EINVAL, "null pointer argument");
+  if (int e = check_aligned({q, k, v, o, dO, dq, dk, dv}, {lse})) return e;
   long long Sp = 0;
   int rc = padded_len(S, n_hosts, &Sp);
   if (rc) return rc;

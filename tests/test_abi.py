@@ -138,6 +138,29 @@ def test_ffn_argument_validation(lib):
                                  512, 256, 512, 256, 3, NULL) == RA_EINVAL
 
 
+def test_misaligned_pointers_are_rejected(lib):
+    """Row tensors are accessed with 16-byte vector loads and stores from their start, so
+    they must begin on a 16-byte boundary; lse needs 4 bytes.  Either is rejected with
+    RA_EINVAL before any device work."""
+    MIS16, MIS4 = ctypes.c_void_p(0x1008), ctypes.c_void_p(0x1002)
+    assert lib.ring_attn_fwd(MIS16, FAKE, FAKE, FAKE, FAKE, 1, 1, 1024, 128, 4, 1, NULL) == RA_EINVAL
+    assert b"16-byte" in lib.ring_attn_last_error()
+    assert lib.ring_attn_fwd(FAKE, FAKE, FAKE, FAKE, MIS4, 1, 1, 1024, 128, 4, 1, NULL) == RA_EINVAL
+    assert b"4-byte" in lib.ring_attn_last_error()
+    assert lib.ring_attn_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, MIS16, FAKE,
+                             1, 1, 1024, 128, 4, 1, NULL) == RA_EINVAL
+    assert lib.ring_attn_bwd_host(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, MIS16,
+                                  1, 1, 1024, 128, 4, 1, 1, NULL) == RA_EINVAL
+    assert lib.ring_attn_decode(FAKE, FAKE, FAKE, MIS16, FAKE, 1, 2, 4096, 128, 1, 8, 1, NULL) == RA_EINVAL
+    assert lib.ring_attn_decode_noalloc(FAKE, MIS16, FAKE, FAKE, FAKE, 1, 2, 4096, 128, 1, 8, 1, NULL) == RA_EINVAL
+    assert lib.blockwise_ffn(FAKE, FAKE, MIS16, FAKE, NULL, FAKE, 512, 256, 512, 256, 0, NULL) == RA_EINVAL
+    assert lib.blockwise_linear(FAKE, FAKE, NULL, MIS16, 512, 256, 256, 256, NULL) == RA_EINVAL
+    P9 = (ctypes.c_void_p * 9)(*([0x1000] * 8 + [0x1008]))
+    assert lib.llama_layer_fwd(FAKE, ctypes.cast(P9, ctypes.c_void_p), FAKE, 1024, 256, 2, 512, 4, 1,
+                               NULL) == RA_EINVAL
+    assert lib.rope_apply(MIS16, 16, 2, 8, 0, 0, NULL) == RA_EINVAL
+
+
 def test_product_path_does_not_use_the_oracle():
     """The package never imports the CPU oracle (it would be a silent CPU fallback)."""
     pkg = os.path.join(ROOT, "paper_2310_01889_amd")
