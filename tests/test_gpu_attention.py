@@ -95,13 +95,15 @@ def test_bf16_forward_invariant_to_block_order():
         assert max_err(lse, lse_ref) <= TOL_O
 
 
-@pytest.mark.parametrize("S,N,causal,full,B", [(16384, 1, 1, True, 1), (32768, 2, 1, False, 1),
-                                               (32768, 2, 0, False, 1), (32768, 2, 1, False, 2)])
-def test_bf16_forward_long_blocks(S, N, causal, full, B):
-    """Blocks of 16384 keys or more run the eight-wave kernel (256 queries per workgroup):
-    a whole head in full on one case (diagonal tiles of every workgroup), otherwise one
-    sampled row of every 32-row wave tile of both heads (of every batch) plus the block edges."""
-    H, D = 2, 128
+@pytest.mark.parametrize("S,N,causal,full,B,D", [(16384, 1, 1, True, 1, 128), (32768, 2, 1, False, 1, 128),
+                                                 (32768, 2, 0, False, 1, 128), (32768, 2, 1, False, 2, 128),
+                                                 (16384, 1, 1, True, 1, 64), (32768, 2, 1, False, 1, 64)])
+def test_bf16_forward_long_blocks(S, N, causal, full, B, D):
+    """Blocks of 16384 keys or more: with D = 128 they run the eight-wave kernel (256 queries
+    per workgroup), with D = 64 the four-wave kernel over as many key tiles.  A whole head in
+    full on the first case of each (diagonal tiles of every workgroup), otherwise one sampled
+    row of every 32-row wave tile of both heads (of every batch) plus the block edges."""
+    H = 2
     q, k, v = synth.attention_inputs(13, B, S, H, D)
     o, lse = ra.attention_fwd(*dev(q, k, v), N, causal)
     torch.cuda.synchronize()
@@ -121,7 +123,7 @@ def test_bf16_forward_long_blocks(S, N, causal, full, B):
         o_ref, lse_ref = OA.attention_rows(q[:, :, hs], k[:, :, hs], v[:, :, hs], rows, bool(causal))
         worst[0] = max(worst[0], max_err(o[:, rows, hs], o_ref))
         worst[1] = max(worst[1], max_err(lse[:, hs][:, :, rows], lse_ref))
-    log("  S=%d N=%d causal=%d: o %.3e lse %.3e" % (S, N, causal, worst[0], worst[1]))
+    log("  S=%d N=%d causal=%d D=%d: o %.3e lse %.3e" % (S, N, causal, D, worst[0], worst[1]))
     assert worst[0] <= TOL_O and worst[1] <= TOL_O
 
 
