@@ -238,6 +238,23 @@ def test_bf16_varlen_causal_forward_backward(S, N, D):
     assert all(torch.equal(a, b) for a, b in zip((dq, dk, dv), g2))
 
 
+@pytest.mark.parametrize("D", [64, 128])
+def test_bf16_backward_long_blocks(D):
+    """Whole-ring backward over two hosts of 16384 keys (S = 32768, one head): dq, dk, dv
+    compared in full; D = 64 runs the one-wave dK/dV kernel, D = 128 the split one."""
+    B, S, H, N = 1, 32768, 1, 2
+    log("bwd long-block case S=%d N=%d D=%d" % (S, N, D))
+    q, k, v, do = synth.attention_inputs(15, B, S, H, D, with_grad=True)
+    qd, kd, vd, dod = dev(q, k, v, do)
+    o, lse = ra.attention_fwd(qd, kd, vd, N, True)
+    dq, dk, dv = ra.attention_bwd(qd, kd, vd, o, lse, dod, N, True)
+    torch.cuda.synchronize()
+    ref = OA.attention_bwd(np64(q), np64(k), np64(v), np64(do), True)
+    errs = [max_err(g, r) for g, r in zip((dq, dk, dv), ref)]
+    log("  max|dq,dk,dv err| %s" % ["%.3e" % e for e in errs])
+    assert max(errs) <= TOL_G
+
+
 def test_bf16_backward_d64_batch2():
     B, S, H, D, N = 2, 512, 3, 64, 4
     q, k, v, do = synth.attention_inputs(10, B, S, H, D, with_grad=True)
