@@ -429,7 +429,7 @@ def main():
                    "global_batch": B, "seq_len": S, "parallelism": "virtual ring of 8 hosts on 1 GPU"},
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "tokens_per_s": round(B * S / (ms * 1e-3), 1),
-        "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128> (attention step)",
+        "roofline": {"bound": "mfma", "kernel": "fwd_bf16_kernel<128, 4> (attention step, four-wave workgroups)",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(),
                      "avg_launch_ms": round(k_avg_ms, 4), "launches": launches,
