@@ -1,0 +1,68 @@
+"""Concurrent calls from two host threads, each on its own stream (default priority).
+
+The library's workspace pool, its side stream (one host's share) and its thread-local error
+text are shared by both threads.  Each thread repeats a whole-ring forward and a one-host-
+share forward on its own inputs; every result must equal, bit for bit, the result of the
+same call made alone beforehand (the kernels are deterministic).
+"""
+import threading
+
+import pytest
+import torch
+
+import paper_2310_01889_amd as ra
+from paper_2310_01889_amd import synth
+from tests.gpu_util import dev, log
+
+pytestmark = pytest.mark.gpu
+
+B, S, H, D = 1, 4096, 4, 128
+CASES = [(4, 3), (8, 7)]  # (n_hosts, host of the share) per thread
+REPS = 6
+
+
+def _calls(qd, kd, vd, n_hosts, host, stream=None):
+    o = torch.empty_like(qd)
+    lse = torch.empty((B, H, S), dtype=torch.float32, device="cuda")
+    ra.ring_attn_fwd(qd, kd, vd, o, lse, n_hosts, True, stream=stream)
+    c = S // n_hosts
+    qb = qd[:, host * c:(host + 1) * c].contiguous()
+    ob = torch.empty_like(qb)
+    lb = torch.empty((B, H, c), dtype=torch.float32, device="cuda")
+    ra.ring_attn_fwd_host(qb, kd, vd, ob, lb, n_hosts, host, True, stream=stream)
+    return o, lse, ob, lb
+
+
+def test_two_threads_two_streams_match_serial_calls():
+    inputs = [dev(*synth.attention_inputs(40 + i, B, S, H, D)) for i in range(len(CASES))]
+    refs = [tuple(t.clone() for t in _calls(*inputs[i], *CASES[i])) for i in range(len(CASES))]
+    torch.cuda.synchronize()
+
+    results = [None] * len(CASES)
+    errors = []
+
+    def work(i):
+        try:
+            st = torch.cuda.Stream()
+            st.wait_stream(torch.cuda.current_stream())
+            outs = []
+            with torch.cuda.stream(st):
+                for _ in range(REPS):
+                    outs.append(_calls(*inputs[i], *CASES[i], stream=st))
+            st.synchronize()
+            results[i] = outs
+        except Exception as e:  # reported below, in the main thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(len(CASES))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a worker thread did not finish"
+    assert not errors, errors
+    for i, outs in enumerate(results):
+        for rep, got in enumerate(outs):
+            for a, b in zip(got, refs[i]):
+                assert torch.equal(a, b), (i, rep)
+    log("  %d threads x %d repetitions: bit-identical to the serial calls" % (len(CASES), REPS))
