@@ -3,9 +3,10 @@
 A whole-ring forward + backward (step kernels only: the key/value exchange happens inside
 them) and one host's share forward (copies on the library's side stream, forked from and
 joined back to the captured stream by events) are captured once, with the workspace
-allocated and freed inside the graph.  The graph is replayed several times, with eager work
-and synchronizations between replays and the outputs cleared by a fill kernel before each;
-every replay must equal the eager result bit for bit.
+allocated and freed inside the graph; so are the two ring-decode calls of a serving loop
+(with workspace, and with the library's fixed scratch array).  The graph is replayed several
+times, with eager work and synchronizations between replays and the outputs cleared by a
+fill kernel before each; every replay must equal the eager result bit for bit.
 """
 import pytest
 import torch
@@ -62,3 +63,38 @@ def test_capture_and_replay_match_eager():
         for i, (a, b) in enumerate(zip(outs, ref)):
             assert torch.equal(a, b), (rep, i)
     log("  4 replays bit-identical to the eager calls")
+
+
+def test_decode_capture_and_replay_match_eager():
+    Bd, Sd, Hd, Dd, Tq, Nd = 2, 8192, 4, 128, 4, 8
+    q, k, v = dev(*synth.attention_inputs(61, Bd, Tq, Hd, Dd, kv_len=Sd))
+    mk = lambda: (torch.empty_like(q), torch.empty((Bd, Hd, Tq), dtype=torch.float32, device="cuda"))
+
+    def run(outs):
+        ra.ring_attn_decode(q, k, v, *outs[0], Nd, True)
+        ra.ring_attn_decode_noalloc(q, k, v, *outs[1], Nd, True)
+    ref = [mk(), mk()]
+    run(ref)
+    torch.cuda.synchronize()
+    outs = [mk(), mk()]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        run(outs)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        run(outs)
+    for rep in range(4):
+        for pair in outs:
+            for t in pair:
+                t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        x = torch.randn(512, 512, device="cuda")
+        (x @ x).sum().item()
+        for a, b in zip([t for p in outs for t in p], [t for p in ref for t in p]):
+            assert torch.equal(a, b), rep
+    log("  decode: 4 replays bit-identical to the eager calls")
