@@ -38,10 +38,7 @@
  *   - Calls are asynchronous and stream-ordered on `stream` (a hipStream_t; NULL means
  *     the legacy default stream).  Work on a side stream is joined back to `stream`
  *     by events, so callers see single-stream semantics.  Distinct streams may be used
- *     from distinct threads concurrently.  The calls may be captured into a HIP graph by
- *     stream capture of `stream` (the workspace then becomes the graph's allocation and free
- *     nodes; the side stream joins and leaves the capture through those events) and the
- *     graph replayed.
+ *     from distinct threads concurrently.
  *   - Workspace (receive buffers, float32 accumulators) is allocated stream-ordered on
  *     `stream` from a memory pool the library owns on each device, and freed back to that
  *     pool at the end of the call (stream-ordered).  The pool keeps freed memory cached for
